@@ -1,0 +1,165 @@
+"""Benchmark: images/s of one CNN partition forward on one MI355X.
+
+Default workload: ResNet-50 layers [44, 56) (layer4 + global avgpool + FC-1000
++ softmax) on 8 x 1024 x 14 x 14 bf16 activations drawn from ReLU(N(0,1)),
+seeded synthetic weights.  A step is one forward of the whole range at the
+workload's batch, inputs resident in HBM.  Prints one JSON line with the
+throughput, the roofline position of the dominant kernel (per-launch HIP
+event timing on the stream the kernels run on) and the CPU oracle timed on
+a bounded sample as a baseline.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "CNN-partition images/sec at batch 1–64; per-layer MFMA % or HBM GB/s"
+PEAK_MFMA_TFLOPS = {"f16": 2516.6, "bf16": 2516.6, "f32": 157.3}
+PEAK_HBM_GBS = 8000.0
+DTYPE_LABEL = {"f32": "f32", "f16": "f16", "bf16": "bf16"}
+
+
+def roofline(records, dtype):
+    """Dominant kernel (largest total time per step) and its position."""
+    groups = {}
+    for r in records:
+        g = groups.setdefault(r["kernel"], {"us": 0.0, "flops": 0.0, "bytes": 0.0, "n": 0})
+        g["us"] += r["mean_us"]
+        g["flops"] += r["flops"]
+        g["bytes"] += r["bytes"]
+        g["n"] += 1
+    name, g = max(groups.items(), key=lambda kv: kv[1]["us"])
+    t_mfma = g["flops"] / (PEAK_MFMA_TFLOPS[dtype] * 1e12)
+    t_hbm = g["bytes"] / (PEAK_HBM_GBS * 1e9)
+    avg_us = g["us"] / g["n"]
+    if t_mfma >= t_hbm:
+        achieved = g["flops"] / g["n"] / (avg_us * 1e-6) / 1e12
+        out = {"bound": "mfma", "achieved": achieved, "peak": PEAK_MFMA_TFLOPS[dtype],
+               "unit": "TFLOP/s"}
+    else:
+        achieved = g["bytes"] / g["n"] / (avg_us * 1e-6) / 1e9
+        out = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
+    out["frac"] = out["achieved"] / out["peak"]
+    out["traffic"] = None
+    out["kernel"] = name
+    out["launches_per_step"] = g["n"]
+    out["avg_launch_us"] = avg_us
+    out["share_of_step"] = g["us"] / sum(v["us"] for v in groups.values())
+    return out
+
+
+def cpu_baseline(wl, m, P, target_s):
+    import oracle
+    x = wl.input(wl.batch)
+    images, t0 = 0, time.perf_counter()
+    while True:
+        oracle.forward(m.layers, P, wl.begin, wl.end, x, wl.dtype)
+        images += wl.batch
+        el = time.perf_counter() - t0
+        if el >= target_s:
+            break
+    return {"value": images / el, "unit": "images/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"{images} images ({images // wl.batch} x the batch of {wl.batch}), "
+                      f"{el:.1f} s wall"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--workload", default="resnet50_layer4_head")
+    ap.add_argument("--batch", type=int, default=0, help="override the workload batch")
+    ap.add_argument("--no-graph", action="store_true", help="launch kernels directly")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="oracle sample length for cpu_baseline (0 disables)")
+    ap.add_argument("--profile-reps", type=int, default=50)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: the partition forward is measured on a single "
+              "MI355X (data parallelism over more GPUs needs no exchange and is not "
+              "launched here)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import workloads as W
+    from paper_2507_18748_amd import Partition
+
+    wl = W.workload(args.workload)
+    if args.batch:
+        import dataclasses
+        wl = dataclasses.replace(wl, batch=args.batch)
+    m = wl.build_model()
+    P = wl.params(m)
+    torch.cuda.set_device(0)
+    part = Partition(m.layers, P, (m.in_c, m.in_h, m.in_w), wl.begin, wl.end, wl.dtype,
+                     max_batch=wl.batch)
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[wl.dtype]
+    x = wl.input(wl.batch)
+    xd = torch.from_numpy(np.ascontiguousarray(x.transpose(0, 2, 3, 1))).to(tdt).cuda()
+    info = part.info
+    odt = torch.float32 if info["out_dtype"] == 0 else tdt
+    out = torch.empty((wl.batch, info["out_h"], info["out_w"], info["out_c"]), dtype=odt,
+                      device="cuda")
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    if not args.no_graph:
+        part.capture(wl.batch, xd.data_ptr(), out.data_ptr())
+    for _ in range(args.warmup):
+        part.run(wl.batch, xd.data_ptr(), out.data_ptr(), sp)
+    torch.cuda.synchronize()
+    print(f"[bench] {wl.name} batch {wl.batch}: warmup done", file=sys.stderr, flush=True)
+
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        part.run(wl.batch, xd.data_ptr(), out.data_ptr(), sp)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    assert torch.isfinite(out.float()).all()
+    print(f"[bench] timed {args.steps} steps: wall {wall * 1e3:.2f} ms, events {gpu_ms:.2f} ms",
+          file=sys.stderr, flush=True)
+
+    recs = part.profile_kernels(wl.batch, warmup=10, reps=args.profile_reps)
+    roof = roofline(recs, wl.dtype)
+    print(f"[bench] dominant kernel {roof['kernel']}: {roof['achieved']:.1f} {roof['unit']} "
+          f"({roof['frac'] * 100:.1f}% of peak)", file=sys.stderr, flush=True)
+
+    result = {
+        "metric": METRIC,
+        "value": wl.batch * args.steps / wall,
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": DTYPE_LABEL[wl.dtype],
+        "data": "synthetic (seeded He-init weights, seeded inputs; no trained weights)",
+        "config": {"workload": wl.description, "name": wl.name, "layers": [wl.begin, wl.end],
+                   "batch": wl.batch, "input": "x".join(map(str, (wl.batch,) + wl.in_chw)) +
+                   f" {wl.dtype} {wl.input_kind}", "graph": not args.no_graph},
+        "roofline": roof,
+    }
+    if args.cpu_seconds > 0:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = cpu_baseline(wl, m, P, args.cpu_seconds)
+    part.close()
+    print(json.dumps(result))
+
+
+if __name__ == "__main__":
+    main()

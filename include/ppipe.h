@@ -1,0 +1,194 @@
+/*
+ * ppipe.h -- C ABI of the MI355X partition-forward library.
+ *
+ * A pipeline partition is the contiguous range of fused layers [begin, end)
+ * of a CNN, "layers i to j (exclusive)" in the paper's MILP inputs (Appendix
+ * A.1, table of inputs, C_ldbij and X_ldbij).  The library runs that range at
+ * a batch size b on one GPU (the batched inference each GPU of a pool
+ * performs, Sec. 2 and Sec. 3) and measures the per-layer latency table
+ * L_kbi and feature-map sizes S_i that the planner consumes (Sec. 3 "Inputs",
+ * Sec. 5.1 offline phase, Sec. 5.2: partition latency is the sum of its
+ * constituent latencies).
+ *
+ * Conventions shared by every call:
+ *  - Activations are NHWC, densely packed, in the partition's storage dtype.
+ *  - Host parameter arrays are fp32; weights use the OIHW layout of the
+ *    framework that defined the model ([out][in] for fully connected layers,
+ *    whose input index follows the (c, h, w) flattening of the producer's
+ *    output).  The library repacks them at create time.
+ *  - A "layer" is fused: a convolution carries its batch norm, bias,
+ *    residual add and activation.  Layer indices are global to the model.
+ *  - Failing calls return NULL or a negative status and leave a message for
+ *    ppipe_last_error() in the calling thread.  No call aborts the process.
+ *  - A handle is not thread-safe; distinct handles are independent.
+ */
+#ifndef PPIPE_H
+#define PPIPE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { PPIPE_F32 = 0, PPIPE_F16 = 1, PPIPE_BF16 = 2 } ppipe_dtype;
+
+typedef enum {
+    PPIPE_OP_CONV = 0,           /* k x k convolution, groups 1 or depthwise (groups = c_in = c_out) */
+    PPIPE_OP_MAXPOOL = 1,        /* k x k window, stride, padding that never wins the max */
+    PPIPE_OP_AVGPOOL_GLOBAL = 2, /* mean over H x W, output 1 x 1 */
+    PPIPE_OP_FC = 3,             /* y = act(W x + b) on the flattened input */
+    PPIPE_OP_FC_SOFTMAX = 4      /* p = softmax(W x + b), fp32 output; must be the range's last layer */
+} ppipe_op;
+
+typedef enum { PPIPE_ACT_NONE = 0, PPIPE_ACT_RELU = 1, PPIPE_ACT_RELU6 = 2 } ppipe_act;
+
+typedef enum {
+    PPIPE_OK = 0,
+    PPIPE_E_INVALID = -1,        /* bad argument, shape or batch */
+    PPIPE_E_SPLIT = -2,          /* a tensor other than layer begin-1's output crosses the boundary */
+    PPIPE_E_UNSUPPORTED = -3,    /* layer shape outside what the kernels implement */
+    PPIPE_E_NOMEM = -4,          /* device allocation failed */
+    PPIPE_E_HIP = -5             /* HIP runtime error (launch, event, stream, graph) */
+} ppipe_status;
+
+/* One fused layer.  Host pointers belong to the caller and are read only
+ * during ppipe_partition_create; they may be NULL for layers outside the
+ * created range.  For CONV with batch norm, all four bn_* arrays are given
+ * (length c_out) and the layer computes
+ *     act( (conv(x) + bias - mean) / sqrt(var + bn_eps) * gamma + beta + res ),
+ * else act(conv(x) + bias + res); bias may be NULL (zero). */
+typedef struct {
+    int32_t op;          /* ppipe_op */
+    int32_t src;         /* producer layer index, -1 = model input */
+    int32_t res_src;     /* layer whose output is added before act, -1 = none (CONV only) */
+    int32_t c_in;        /* input channels; for FC the flattened input length */
+    int32_t c_out;
+    int32_t k;           /* square window (CONV, MAXPOOL) */
+    int32_t stride;
+    int32_t pad;
+    int32_t groups;      /* 1, or c_in (== c_out) for depthwise */
+    int32_t act;         /* ppipe_act */
+    const float* weight; /* CONV [c_out][c_in/groups][k][k]; FC [c_out][c_in] */
+    const float* bias;   /* [c_out] or NULL */
+    const float* bn_gamma;
+    const float* bn_beta;
+    const float* bn_mean;
+    const float* bn_var;
+    float bn_eps;
+} ppipe_layer_desc;
+
+/* The whole model (all layers from 0), so shapes can be derived for any
+ * range.  Input is in_c x in_h x in_w per image. */
+typedef struct {
+    int32_t n_layers;
+    const ppipe_layer_desc* layers;
+    int32_t in_c, in_h, in_w;
+    int32_t max_batch;   /* largest batch run() accepts; <= 0 selects 64 */
+} ppipe_model_desc;
+
+typedef struct ppipe_partition ppipe_partition;
+
+typedef struct {
+    int32_t layer_begin, layer_end;  /* the range [begin, end) */
+    int32_t dtype;                   /* ppipe_dtype of activations and weights */
+    int32_t max_batch;
+    int32_t in_c, in_h, in_w;        /* per-image input of the range (NHWC) */
+    int32_t out_c, out_h, out_w;     /* per-image output of the range */
+    int32_t out_dtype;               /* PPIPE_F32 when the range ends with FC_SOFTMAX */
+    int64_t in_bytes_per_image, out_bytes_per_image;
+    int64_t weight_bytes;            /* device bytes of packed weights, scales and biases */
+    int64_t workspace_bytes;         /* device bytes of activation and split-K buffers */
+} ppipe_partition_info_t;
+
+typedef struct {
+    int32_t index;                   /* global layer index */
+    int32_t op;                      /* ppipe_op */
+    int32_t out_c, out_h, out_w;
+    int32_t kernel_count;            /* launches this layer issues at the queried batch */
+    int64_t out_bytes_b1;            /* S_i: output feature-map bytes at batch 1 */
+    double flops_b1;                 /* algorithmic FLOPs at batch 1 (2 per multiply-add) */
+    double act_bytes_b1;             /* input + output (+ residual) activation bytes at batch 1 */
+    double param_bytes;              /* weight bytes in dtype + fp32 scale/bias, once per run */
+    char kernel[96];                 /* kernel configuration chosen at the queried batch */
+} ppipe_layer_info_t;
+
+typedef struct {
+    int32_t layer;                   /* global layer index */
+    int32_t launch;                  /* 0-based launch number within the layer */
+    char kernel[96];                 /* kernel configuration */
+    double flops;                    /* algorithmic FLOPs attributed to this launch */
+    double bytes;                    /* algorithmic HBM bytes attributed to this launch */
+    float mean_us, median_us, min_us;
+} ppipe_kernel_record;
+
+/* Build a partition of layers [layer_begin, layer_end) of desc in dtype.
+ * Validates the range and every layer shape, folds batch norm into fp32
+ * per-channel scale and bias, repacks weights to the kernels' layout in
+ * dtype, and allocates device weights plus activation and split-K buffers
+ * sized for desc->max_batch.  Returns NULL on error (PPIPE_E_SPLIT when a
+ * layer in the range reads a tensor produced before layer_begin other than
+ * layer_begin-1's output, or a layer after the range reads one produced
+ * inside it other than layer_end-1's output).  Uses the current HIP device. */
+ppipe_partition* ppipe_partition_create(const ppipe_model_desc* desc,
+                                        int32_t layer_begin, int32_t layer_end,
+                                        int32_t dtype);
+
+/* Forward pass of the range at batch size `batch` (1..max_batch).
+ * in:  device pointer, [batch][in_h][in_w][in_c] in dtype (caller-owned).
+ * out: device pointer, [batch][out_h][out_w][out_c] in out_dtype (caller-owned);
+ *      [batch][classes] fp32 probabilities when the range ends with FC_SOFTMAX.
+ * stream: a hipStream_t (NULL = default stream).  Asynchronous: enqueues work
+ * on the stream and returns; no host synchronisation, no allocation.  If a
+ * graph for (batch, in, out) was captured with ppipe_partition_capture it is
+ * replayed, otherwise the kernels are launched directly.  Concurrent runs of
+ * one handle on different streams race on its buffers. */
+int ppipe_partition_run(ppipe_partition* h, int32_t batch, const void* in,
+                        void* out, void* stream);
+
+/* Record the launches run() would issue for (batch, in, out) into a HIP
+ * graph (host-side work only; allocates graph objects).  Later runs with the
+ * same triple replay it.  Returns a status. */
+int ppipe_partition_capture(ppipe_partition* h, int32_t batch, const void* in,
+                            void* out);
+
+/* Per-layer latency table: for each batch_sizes[j], `warmup` untimed runs,
+ * then `reps` runs with a HIP event before every layer and after the last on
+ * a private stream; out_us[i * n_batches + j] = median microseconds of layer
+ * begin + i, out_partition_us[j] = median of the whole range timed without
+ * the per-layer events (either output may be NULL).  Allocates its own input
+ * and output buffers, synchronises internally.  Returns a status. */
+int ppipe_profile_layers(ppipe_partition* h, const int32_t* batch_sizes,
+                         int32_t n_batches, int32_t warmup, int32_t reps,
+                         float* out_us, float* out_partition_us);
+
+/* Per-launch timing at one batch: like ppipe_profile_layers but with events
+ * around every kernel launch.  Writes up to `capacity` records, sets *count
+ * to the number of launches per run.  Returns a status. */
+int ppipe_profile_kernels(ppipe_partition* h, int32_t batch, int32_t warmup,
+                          int32_t reps, ppipe_kernel_record* records,
+                          int32_t capacity, int32_t* count);
+
+int ppipe_partition_info(const ppipe_partition* h, ppipe_partition_info_t* info);
+
+/* Static description of global layer `index` (begin <= index < end) with the
+ * kernel choice and launch count at `batch`. */
+int ppipe_layer_info(const ppipe_partition* h, int32_t index, int32_t batch,
+                     ppipe_layer_info_t* info);
+
+/* Free every device and host resource of the handle.  NULL is a no-op.  The
+ * caller must ensure no run() on the handle is still executing. */
+void ppipe_partition_destroy(ppipe_partition* h);
+
+/* Message of the last failing call in this thread ("" if none). */
+const char* ppipe_last_error(void);
+
+/* ppipe_status of the last failing call in this thread (0 if none); the way
+ * to tell why ppipe_partition_create returned NULL. */
+int32_t ppipe_last_status(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PPIPE_H */

@@ -1,0 +1,227 @@
+"""ctypes binding of libppipe.so: argument marshalling only.
+
+Every step of the forward pass runs in the library's HIP kernels; PyTorch is
+used by callers only for device memory (tensor.data_ptr()) and streams
+(torch.cuda.Stream.cuda_stream).  The binding raises when the library is not
+built: there is no fallback implementation.
+"""
+import ctypes
+import os
+from typing import Dict, Iterable, List, Optional, Sequence
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libppipe.so")
+
+OPS = {"conv": 0, "maxpool": 1, "gap": 2, "fc": 3, "fc_softmax": 4}
+ACTS = {"none": 0, "relu": 1, "relu6": 2}
+DTYPES = {"f32": 0, "f16": 1, "bf16": 2}
+
+_fp = ctypes.POINTER(ctypes.c_float)
+
+
+class LayerDesc(ctypes.Structure):
+    _fields_ = [("op", ctypes.c_int32), ("src", ctypes.c_int32), ("res_src", ctypes.c_int32),
+                ("c_in", ctypes.c_int32), ("c_out", ctypes.c_int32), ("k", ctypes.c_int32),
+                ("stride", ctypes.c_int32), ("pad", ctypes.c_int32), ("groups", ctypes.c_int32),
+                ("act", ctypes.c_int32), ("weight", _fp), ("bias", _fp), ("bn_gamma", _fp),
+                ("bn_beta", _fp), ("bn_mean", _fp), ("bn_var", _fp), ("bn_eps", ctypes.c_float)]
+
+
+class ModelDesc(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("layers", ctypes.POINTER(LayerDesc)),
+                ("in_c", ctypes.c_int32), ("in_h", ctypes.c_int32), ("in_w", ctypes.c_int32),
+                ("max_batch", ctypes.c_int32)]
+
+
+class PartitionInfo(ctypes.Structure):
+    _fields_ = [("layer_begin", ctypes.c_int32), ("layer_end", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("max_batch", ctypes.c_int32),
+                ("in_c", ctypes.c_int32), ("in_h", ctypes.c_int32), ("in_w", ctypes.c_int32),
+                ("out_c", ctypes.c_int32), ("out_h", ctypes.c_int32), ("out_w", ctypes.c_int32),
+                ("out_dtype", ctypes.c_int32), ("in_bytes_per_image", ctypes.c_int64),
+                ("out_bytes_per_image", ctypes.c_int64), ("weight_bytes", ctypes.c_int64),
+                ("workspace_bytes", ctypes.c_int64)]
+
+
+class LayerInfo(ctypes.Structure):
+    _fields_ = [("index", ctypes.c_int32), ("op", ctypes.c_int32), ("out_c", ctypes.c_int32),
+                ("out_h", ctypes.c_int32), ("out_w", ctypes.c_int32),
+                ("kernel_count", ctypes.c_int32), ("out_bytes_b1", ctypes.c_int64),
+                ("flops_b1", ctypes.c_double), ("act_bytes_b1", ctypes.c_double),
+                ("param_bytes", ctypes.c_double), ("kernel", ctypes.c_char * 96)]
+
+
+class KernelRecord(ctypes.Structure):
+    _fields_ = [("layer", ctypes.c_int32), ("launch", ctypes.c_int32),
+                ("kernel", ctypes.c_char * 96), ("flops", ctypes.c_double),
+                ("bytes", ctypes.c_double), ("mean_us", ctypes.c_float),
+                ("median_us", ctypes.c_float), ("min_us", ctypes.c_float)]
+
+
+STATUS = {0: "OK", -1: "INVALID", -2: "SPLIT", -3: "UNSUPPORTED", -4: "NOMEM", -5: "HIP"}
+
+
+class PpipeError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"ppipe error {status} ({STATUS.get(status, '?')}): {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def load_library() -> ctypes.CDLL:
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise PpipeError(-5, f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                              "or python paper_2507_18748_amd/build.py")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32 = ctypes.c_void_p, ctypes.c_int32
+    lib.ppipe_partition_create.restype = vp
+    lib.ppipe_partition_create.argtypes = [ctypes.POINTER(ModelDesc), i32, i32, i32]
+    lib.ppipe_partition_run.restype = ctypes.c_int
+    lib.ppipe_partition_run.argtypes = [vp, i32, vp, vp, vp]
+    lib.ppipe_partition_capture.restype = ctypes.c_int
+    lib.ppipe_partition_capture.argtypes = [vp, i32, vp, vp]
+    lib.ppipe_profile_layers.restype = ctypes.c_int
+    lib.ppipe_profile_layers.argtypes = [vp, ctypes.POINTER(i32), i32, i32, i32, _fp, _fp]
+    lib.ppipe_profile_kernels.restype = ctypes.c_int
+    lib.ppipe_profile_kernels.argtypes = [vp, i32, i32, i32, ctypes.POINTER(KernelRecord), i32,
+                                          ctypes.POINTER(i32)]
+    lib.ppipe_partition_info.restype = ctypes.c_int
+    lib.ppipe_partition_info.argtypes = [vp, ctypes.POINTER(PartitionInfo)]
+    lib.ppipe_layer_info.restype = ctypes.c_int
+    lib.ppipe_layer_info.argtypes = [vp, i32, i32, ctypes.POINTER(LayerInfo)]
+    lib.ppipe_partition_destroy.restype = None
+    lib.ppipe_partition_destroy.argtypes = [vp]
+    lib.ppipe_last_error.restype = ctypes.c_char_p
+    lib.ppipe_last_error.argtypes = []
+    lib.ppipe_last_status.restype = ctypes.c_int32
+    lib.ppipe_last_status.argtypes = []
+    _lib = lib
+    return lib
+
+
+def _err(lib, status: int):
+    return PpipeError(status, lib.ppipe_last_error().decode(errors="replace"))
+
+
+def _attr(L, name, default=None):
+    return L[name] if isinstance(L, dict) else getattr(L, name, default)
+
+
+class Partition:
+    """Layers [begin, end) of a model on the current HIP device.
+
+    layers: sequence of objects (or dicts) with fields op, src, res_src, c_in,
+      c_out, k, stride, pad, groups, act (op / act as names, see OPS / ACTS).
+    params: {layer index: {"weight", "bias", "bn_gamma", "bn_beta", "bn_mean",
+      "bn_var"}} of float32 numpy arrays (OIHW weights); read during create.
+    """
+
+    def __init__(self, layers: Sequence, params: Dict[int, Dict[str, np.ndarray]],
+                 in_chw: Sequence[int], begin: int, end: int, dtype: str,
+                 max_batch: int = 64, bn_eps: float = 1e-5):
+        self._lib = load_library()
+        self.begin, self.end, self.dtype = begin, end, dtype
+        keep: List[np.ndarray] = []
+
+        def ptr(a: Optional[np.ndarray]):
+            if a is None:
+                return None
+            a = np.ascontiguousarray(a, dtype=np.float32)
+            keep.append(a)
+            return a.ctypes.data_as(_fp)
+
+        arr = (LayerDesc * len(layers))()
+        for i, L in enumerate(layers):
+            d = arr[i]
+            d.op = OPS[_attr(L, "op")]
+            d.src = _attr(L, "src")
+            d.res_src = _attr(L, "res_src", -1)
+            d.c_in, d.c_out = _attr(L, "c_in"), _attr(L, "c_out")
+            d.k, d.stride = _attr(L, "k", 1), _attr(L, "stride", 1)
+            d.pad, d.groups = _attr(L, "pad", 0), _attr(L, "groups", 1)
+            d.act = ACTS[_attr(L, "act", "none")]
+            d.bn_eps = bn_eps
+            p = params.get(i, {}) if begin <= i < end else {}
+            d.weight = ptr(p.get("weight"))
+            d.bias = ptr(p.get("bias"))
+            d.bn_gamma = ptr(p.get("bn_gamma"))
+            d.bn_beta = ptr(p.get("bn_beta"))
+            d.bn_mean = ptr(p.get("bn_mean"))
+            d.bn_var = ptr(p.get("bn_var"))
+        desc = ModelDesc(len(layers), arr, int(in_chw[0]), int(in_chw[1]), int(in_chw[2]),
+                         int(max_batch))
+        h = self._lib.ppipe_partition_create(ctypes.byref(desc), begin, end, DTYPES[dtype])
+        if not h:
+            raise _err(self._lib, self._lib.ppipe_last_status())
+        self._h = ctypes.c_void_p(h)
+        info = PartitionInfo()
+        self._check(self._lib.ppipe_partition_info(self._h, ctypes.byref(info)))
+        self.info = {f: getattr(info, f) for f, _ in PartitionInfo._fields_}
+
+    def _check(self, status: int):
+        if status != 0:
+            raise _err(self._lib, status)
+
+    # --- execution ---
+    def run(self, batch: int, x_ptr: int, out_ptr: int, stream: int = 0):
+        """x_ptr / out_ptr: device addresses (tensor.data_ptr()); stream: hipStream_t."""
+        self._check(self._lib.ppipe_partition_run(self._h, batch, x_ptr, out_ptr, stream))
+
+    def capture(self, batch: int, x_ptr: int, out_ptr: int):
+        self._check(self._lib.ppipe_partition_capture(self._h, batch, x_ptr, out_ptr))
+
+    # --- profiling ---
+    def profile_layers(self, batch_sizes: Iterable[int], warmup: int = 10, reps: int = 50):
+        bs = list(batch_sizes)
+        nl = self.end - self.begin
+        b_arr = (ctypes.c_int32 * len(bs))(*bs)
+        table = np.zeros((nl, len(bs)), dtype=np.float32)
+        whole = np.zeros(len(bs), dtype=np.float32)
+        self._check(self._lib.ppipe_profile_layers(self._h, b_arr, len(bs), warmup, reps,
+                                                   table.ctypes.data_as(_fp),
+                                                   whole.ctypes.data_as(_fp)))
+        return table, whole
+
+    def profile_kernels(self, batch: int, warmup: int = 10, reps: int = 50) -> List[dict]:
+        count = ctypes.c_int32(0)
+        cap = 4 * (self.end - self.begin) + 8
+        recs = (KernelRecord * cap)()
+        self._check(self._lib.ppipe_profile_kernels(self._h, batch, warmup, reps, recs, cap,
+                                                    ctypes.byref(count)))
+        out = []
+        for r in recs[:min(count.value, cap)]:
+            out.append({"layer": r.layer, "launch": r.launch, "kernel": r.kernel.decode(),
+                        "flops": r.flops, "bytes": r.bytes, "mean_us": r.mean_us,
+                        "median_us": r.median_us, "min_us": r.min_us})
+        return out
+
+    def layer_info(self, index: int, batch: int = 1) -> dict:
+        li = LayerInfo()
+        self._check(self._lib.ppipe_layer_info(self._h, index, batch, ctypes.byref(li)))
+        d = {f: getattr(li, f) for f, _ in LayerInfo._fields_}
+        d["kernel"] = li.kernel.decode()
+        return d
+
+    # --- lifetime ---
+    def close(self):
+        if getattr(self, "_h", None):
+            self._lib.ppipe_partition_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()

@@ -1,0 +1,244 @@
+// Memory-bound layers on NHWC activations: depthwise convolution, max pooling
+// and global average pooling.
+//
+// Each thread owns one 16-byte channel vector (8 x 16-bit or 4 x fp32) of one
+// output pixel, so consecutive lanes read and write consecutive 16-byte
+// chunks of the channel dimension (fully coalesced global_load_dwordx4 /
+// global_store_dwordx4).  Arithmetic is fp32; results are rounded once to
+// the storage type.  Window taps that repeat across neighbouring pixels are
+// served by L1/L2; HBM sees each input byte about once.
+#include "kernels.h"
+
+namespace ppipe {
+
+template <typename T> struct Vec16 {  // 16-bit element types: 8 per vector
+    static constexpr int N = 8;
+    static __device__ __forceinline__ void load(const T* p, float* f)
+    {
+        uint4 u = *(const uint4*)p;
+        T e[8];
+        __builtin_memcpy(e, &u, 16);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) f[i] = (float)e[i];
+    }
+    static __device__ __forceinline__ void store(T* p, const float* f)
+    {
+        T e[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) e[i] = (T)f[i];
+        uint4 u;
+        __builtin_memcpy(&u, e, 16);
+        *(uint4*)p = u;
+    }
+};
+template <> struct Vec16<float> {
+    static constexpr int N = 4;
+    static __device__ __forceinline__ void load(const float* p, float* f)
+    {
+        float4 v = *(const float4*)p;
+        f[0] = v.x; f[1] = v.y; f[2] = v.z; f[3] = v.w;
+    }
+    static __device__ __forceinline__ void store(float* p, const float* f)
+    {
+        *(float4*)p = make_float4(f[0], f[1], f[2], f[3]);
+    }
+};
+
+__device__ __forceinline__ float act_f(float v, int act)
+{
+    if (act == ACT_RELU) return fmaxf(v, 0.0f);
+    if (act == ACT_RELU6) return fminf(fmaxf(v, 0.0f), 6.0f);
+    return v;
+}
+
+// y[n][ho][wo][c] = act(scale[c] * sum_{kh,kw} x[n][ho*s-p+kh][wo*s-p+kw][c] * w[kh][kw][c] + bias[c])
+template <typename T, int K>
+__global__ void __launch_bounds__(256)
+dwconv_kernel(const T* __restrict__ x, const T* __restrict__ w, const float* __restrict__ scale,
+              const float* __restrict__ bias, T* __restrict__ y, int N, int H, int W, int C,
+              int Ho, int Wo, int stride, int pad, int act)
+{
+    constexpr int V = Vec16<T>::N;
+    const int CV = C / V;
+    const size_t total = (size_t)N * Ho * Wo * CV;
+    const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= total)
+        return;
+    const int cv = (int)(idx % CV);
+    size_t p = idx / CV;
+    const int wo = (int)(p % Wo);
+    p /= Wo;
+    const int ho = (int)(p % Ho);
+    const int n = (int)(p / Ho);
+    const int c = cv * V;
+    float acc[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) acc[i] = 0.0f;
+#pragma unroll
+    for (int kh = 0; kh < K; ++kh) {
+        const int hi = ho * stride - pad + kh;
+        if ((unsigned)hi >= (unsigned)H)
+            continue;
+#pragma unroll
+        for (int kw = 0; kw < K; ++kw) {
+            const int wi = wo * stride - pad + kw;
+            if ((unsigned)wi >= (unsigned)W)
+                continue;
+            float xv[V], wv[V];
+            Vec16<T>::load(x + (((size_t)n * H + hi) * W + wi) * C + c, xv);
+            Vec16<T>::load(w + (size_t)(kh * K + kw) * C + c, wv);
+#pragma unroll
+            for (int i = 0; i < V; ++i) acc[i] = fmaf(xv[i], wv[i], acc[i]);
+        }
+    }
+    float o[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) o[i] = act_f(acc[i] * scale[c + i] + bias[c + i], act);
+    Vec16<T>::store(y + (((size_t)n * Ho + ho) * Wo + wo) * C + c, o);
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+maxpool_kernel(const T* __restrict__ x, T* __restrict__ y, int N, int H, int W, int C, int Ho,
+               int Wo, int k, int stride, int pad)
+{
+    constexpr int V = Vec16<T>::N;
+    const int CV = C / V;
+    const size_t total = (size_t)N * Ho * Wo * CV;
+    const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= total)
+        return;
+    const int cv = (int)(idx % CV);
+    size_t p = idx / CV;
+    const int wo = (int)(p % Wo);
+    p /= Wo;
+    const int ho = (int)(p % Ho);
+    const int n = (int)(p / Ho);
+    const int c = cv * V;
+    float m[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) m[i] = -INFINITY;
+    for (int kh = 0; kh < k; ++kh) {
+        const int hi = ho * stride - pad + kh;
+        if ((unsigned)hi >= (unsigned)H)
+            continue;
+        for (int kw = 0; kw < k; ++kw) {
+            const int wi = wo * stride - pad + kw;
+            if ((unsigned)wi >= (unsigned)W)
+                continue;
+            float v[V];
+            Vec16<T>::load(x + (((size_t)n * H + hi) * W + wi) * C + c, v);
+#pragma unroll
+            for (int i = 0; i < V; ++i) m[i] = fmaxf(m[i], v[i]);
+        }
+    }
+    Vec16<T>::store(y + (((size_t)n * Ho + ho) * Wo + wo) * C + c, m);
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+gap_kernel(const T* __restrict__ x, T* __restrict__ y, int N, int HW, int C)
+{
+    constexpr int V = Vec16<T>::N;
+    const int CV = C / V;
+    const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= (size_t)N * CV)
+        return;
+    const int cv = (int)(idx % CV), n = (int)(idx / CV);
+    float s[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) s[i] = 0.0f;
+    const T* p = x + (size_t)n * HW * C + cv * V;
+    for (int t = 0; t < HW; ++t) {
+        float v[V];
+        Vec16<T>::load(p + (size_t)t * C, v);
+#pragma unroll
+        for (int i = 0; i < V; ++i) s[i] += v[i];
+    }
+    const float inv = 1.0f / (float)HW;
+#pragma unroll
+    for (int i = 0; i < V; ++i) s[i] *= inv;
+    Vec16<T>::store(y + (size_t)n * C + cv * V, s);
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) fill_uniform_kernel(T* p, size_t n, uint32_t seed)
+{
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n)
+        return;
+    uint32_t h = (uint32_t)i * 0x9E3779B1u ^ seed;
+    h ^= h >> 16; h *= 0x85EBCA6Bu; h ^= h >> 13; h *= 0xC2B2AE35u; h ^= h >> 16;
+    p[i] = (T)((float)(h >> 8) * (1.0f / 16777216.0f));
+}
+
+static unsigned blocks_for(size_t n) { return (unsigned)((n + 255) / 256); }
+
+#define PPIPE_DISPATCH(dt, KERNEL_CALL)                                   \
+    switch (dt) {                                                         \
+    case DT_F32:  { typedef float T; KERNEL_CALL; break; }                \
+    case DT_F16:  { typedef _Float16 T; KERNEL_CALL; break; }             \
+    case DT_BF16: { typedef __bf16 T; KERNEL_CALL; break; }               \
+    default: return hipErrorInvalidValue;                                 \
+    }
+
+hipError_t launch_dwconv(int dt, const void* x, const void* w, const float* scale,
+                         const float* bias, void* y, int N, int H, int W, int C, int Ho,
+                         int Wo, int k, int stride, int pad, int act, hipStream_t s)
+{
+    if (k != 3)
+        return hipErrorInvalidValue;
+    const size_t total = (size_t)N * Ho * Wo * C / (16 / dtype_size(dt));
+    PPIPE_DISPATCH(dt, hipLaunchKernelGGL((dwconv_kernel<T, 3>), dim3(blocks_for(total)),
+                                          dim3(256), 0, s, (const T*)x, (const T*)w, scale,
+                                          bias, (T*)y, N, H, W, C, Ho, Wo, stride, pad, act));
+    return hipGetLastError();
+}
+
+hipError_t launch_maxpool(int dt, const void* x, void* y, int N, int H, int W, int C,
+                          int Ho, int Wo, int k, int stride, int pad, hipStream_t s)
+{
+    const size_t total = (size_t)N * Ho * Wo * C / (16 / dtype_size(dt));
+    PPIPE_DISPATCH(dt, hipLaunchKernelGGL(maxpool_kernel<T>, dim3(blocks_for(total)),
+                                          dim3(256), 0, s, (const T*)x, (T*)y, N, H, W, C,
+                                          Ho, Wo, k, stride, pad));
+    return hipGetLastError();
+}
+
+hipError_t launch_gap(int dt, const void* x, void* y, int N, int HW, int C, hipStream_t s)
+{
+    const size_t total = (size_t)N * C / (16 / dtype_size(dt));
+    PPIPE_DISPATCH(dt, hipLaunchKernelGGL(gap_kernel<T>, dim3(blocks_for(total)), dim3(256),
+                                          0, s, (const T*)x, (T*)y, N, HW, C));
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_uniform(int dt, void* p, size_t n, uint32_t seed, hipStream_t s)
+{
+    PPIPE_DISPATCH(dt, hipLaunchKernelGGL(fill_uniform_kernel<T>, dim3(blocks_for(n)),
+                                          dim3(256), 0, s, (T*)p, n, seed));
+    return hipGetLastError();
+}
+
+static const char* dtn(int dt) { return dt == DT_F32 ? "f32" : dt == DT_F16 ? "f16" : "bf16"; }
+
+const char* dwconv_name(int dt, int k)
+{
+    static char n[3][48];
+    if (!n[dt][0]) snprintf(n[dt], 48, "dwconv%dx%d<%s>", k, k, dtn(dt));
+    return n[dt];
+}
+const char* maxpool_name(int dt)
+{
+    static char n[3][32];
+    if (!n[dt][0]) snprintf(n[dt], 32, "maxpool<%s>", dtn(dt));
+    return n[dt];
+}
+const char* gap_name(int dt)
+{
+    static char n[3][32];
+    if (!n[dt][0]) snprintf(n[dt], 32, "global_avgpool<%s>", dtn(dt));
+    return n[dt];
+}
+
+}  // namespace ppipe

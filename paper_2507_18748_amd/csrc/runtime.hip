@@ -1,0 +1,971 @@
+// Partition runtime behind the C ABI in include/ppipe.h.
+//
+// create: validates the layer range [begin, end) (a partition spans layers i
+//   to j exclusive and receives only layer i-1's feature map: the paper's
+//   MILP inputs C_ldbij and Y_bj, Appendix A.1), derives every layer shape
+//   from the model input, folds batch norm into fp32 per-channel scale and
+//   shift, repacks weights to the kernels' layouts in the storage dtype,
+//   assigns activation buffers by liveness, chooses a kernel plan for every
+//   (layer, batch) pair and allocates everything once for max_batch.
+// run: walks the range in index order on the caller's stream, or replays a
+//   captured HIP graph; no allocation, no host synchronisation.
+// profile: per-layer and per-launch HIP event timing that produces the
+//   latency table L[i][b] and the feature-map sizes S_i (Sec. 3 inputs,
+//   Sec. 5.1 offline profiling).
+#include "ppipe.h"
+#include "kernels.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+using namespace ppipe;
+
+namespace {
+
+thread_local std::string g_err;
+thread_local int g_status = 0;
+
+int fail(int code, const std::string& msg)
+{
+    g_err = msg;
+    g_status = code;
+    return code;
+}
+
+std::string hip_msg(const char* what, hipError_t e)
+{
+    return std::string(what) + ": " + hipGetErrorString(e);
+}
+
+// ---- host-side rounding for weight packing (fp32 -> 16-bit, nearest even) ----
+uint16_t f32_to_f16_bits(float f)
+{
+    uint32_t x;
+    std::memcpy(&x, &f, 4);
+    const uint32_t sign = (x >> 16) & 0x8000u;
+    const uint32_t ax = x & 0x7fffffffu;
+    if (ax >= 0x7f800000u)                      // inf / nan
+        return (uint16_t)(sign | (ax > 0x7f800000u ? 0x7e00u : 0x7c00u));
+    if (ax >= 0x477ff000u)                      // >= 65520 rounds to inf
+        return (uint16_t)(sign | 0x7c00u);
+    if (ax < 0x38800000u) {                     // below 2^-14: multiples of 2^-24
+        float af;
+        std::memcpy(&af, &ax, 4);
+        return (uint16_t)(sign | (uint32_t)std::nearbyint(af * 16777216.0f));
+    }
+    uint32_t h = ((((ax >> 23) - 127u + 15u) << 10) | ((ax & 0x7fffffu) >> 13));
+    const uint32_t rem = ax & 0x1fffu;
+    if (rem > 0x1000u || (rem == 0x1000u && (h & 1u)))
+        ++h;
+    return (uint16_t)(sign | h);
+}
+
+uint16_t f32_to_bf16_bits(float f)
+{
+    uint32_t x;
+    std::memcpy(&x, &f, 4);
+    if ((x & 0x7fffffffu) > 0x7f800000u)
+        return (uint16_t)((x >> 16) | 0x40u);
+    return (uint16_t)((x + 0x7fffu + ((x >> 16) & 1u)) >> 16);
+}
+
+void put_elem(std::vector<uint8_t>& blob, size_t off, int dt, size_t i, float v)
+{
+    if (dt == DT_F32) {
+        std::memcpy(&blob[off + i * 4], &v, 4);
+    } else {
+        uint16_t b = dt == DT_F16 ? f32_to_f16_bits(v) : f32_to_bf16_bits(v);
+        std::memcpy(&blob[off + i * 2], &b, 2);
+    }
+}
+
+enum Kind { K_GEMM = 0, K_DW = 1, K_MAXPOOL = 2, K_GAP = 3 };
+enum { BUF_IN = -1, BUF_OUT = -2, BUF_NONE = -3 };
+
+struct Plan {
+    int cfg, splits, chunks_per_split, total_chunks;
+};
+
+struct Shape {
+    int c, h, w;
+};
+
+}  // namespace
+
+struct LayerRT {
+    int index, op, src, res_src, act, k, stride, pad, groups;
+    int H, W, C, Ho, Wo, Co;
+    int kind;
+    bool generic = false, softmax = false;
+    int KH = 1, KW = 1, gstride = 1, gpad = 0, K = 0, Kpad = 0;
+    size_t w_off = 0, scale_off = 0, bias_off = 0;
+    void* w = nullptr;
+    float* scale = nullptr;
+    float* bias = nullptr;
+    int in_buf = BUF_IN, res_buf = BUF_NONE, out_buf = BUF_OUT;
+    std::vector<Plan> plans;   // [batch - 1]
+    int64_t out_bytes_b1 = 0;
+    double flops_b1 = 0, in_bytes_b1 = 0, res_bytes_b1 = 0, param_bytes = 0;
+};
+
+struct GraphEntry {
+    int batch;
+    const void* in;
+    void* out;
+    hipGraph_t graph;
+    hipGraphExec_t exec;
+};
+
+struct ppipe_partition {
+    int begin = 0, end = 0, dtype = 0, max_batch = 64, device = 0;
+    Shape in{}, out{};
+    int out_dtype = 0;
+    std::vector<LayerRT> L;
+    std::vector<void*> slots;
+    std::vector<size_t> slot_bytes;
+    float* ws = nullptr;
+    size_t ws_bytes = 0;
+    void* wblob = nullptr;
+    size_t wbytes = 0;
+    std::vector<uint8_t> host_blob;   // packed parameters between validation and upload
+    hipStream_t cap_stream = nullptr;
+    std::vector<GraphEntry> graphs;
+};
+
+namespace {
+
+Plan choose_plan(int M, int Co, int K, int dt)
+{
+    auto tiles = [&](int cfg) {
+        GemmCfgInfo c = gemm_cfg_info(cfg);
+        return (int64_t)((M + c.bn - 1) / c.bn) * ((Co + c.bm - 1) / c.bm);
+    };
+    int cfg;
+    if (M <= 32)
+        cfg = GEMM_64x16;
+    else if (tiles(GEMM_128x128) >= 256)
+        cfg = GEMM_128x128;
+    else
+        cfg = GEMM_64x64;
+    const int bk = gemm_bk(cfg, dt);
+    const int total = (K + bk - 1) / bk;
+    const int64_t t = tiles(cfg);
+    int splits = 1;
+    while (t * splits * 2 <= 512 && total / (splits * 2) >= 8 && splits * 2 <= 32)
+        splits *= 2;
+    const int cps = (total + splits - 1) / splits;
+    splits = (total + cps - 1) / cps;
+    return {cfg, splits, cps, total};
+}
+
+const void* buf_ptr(const ppipe_partition* P, int id, const void* in, void* out)
+{
+    if (id == BUF_IN) return in;
+    if (id == BUF_OUT) return out;
+    if (id == BUF_NONE) return nullptr;
+    return P->slots[id];
+}
+
+// Receives a callback around every kernel launch (profiling).
+struct LaunchHook {
+    virtual ~LaunchHook() = default;
+    virtual void before(const LayerRT&, int, hipStream_t) {}
+    virtual void after(const LayerRT&, int, hipStream_t) {}
+};
+
+int layer_launches(const LayerRT& l, int batch)
+{
+    if (l.kind != K_GEMM) return 1;
+    const Plan& p = l.plans[batch - 1];
+    return (l.softmax || p.splits > 1) ? 2 : 1;
+}
+
+std::string launch_name(const ppipe_partition* P, const LayerRT& l, int batch, int launch)
+{
+    switch (l.kind) {
+    case K_GEMM: {
+        const Plan& p = l.plans[batch - 1];
+        if (launch == 0) {
+            std::string s = conv_gemm_name(P->dtype, p.cfg, l.generic);
+            return s;
+        }
+        return l.softmax ? splitk_softmax_name() : splitk_epilogue_name(P->dtype);
+    }
+    case K_DW: return dwconv_name(P->dtype, l.k);
+    case K_MAXPOOL: return maxpool_name(P->dtype);
+    default: return gap_name(P->dtype);
+    }
+}
+
+// Algorithmic work attributed to one launch: the GEMM launch owns the FLOPs,
+// input and weight bytes; a following reduction owns the output (+ residual).
+void launch_work(const ppipe_partition* P, const LayerRT& l, int batch, int launch,
+                 double* flops, double* bytes)
+{
+    const double b = batch;
+    const double out_bytes = b * (double)l.out_bytes_b1 *
+                             (l.softmax ? 4.0 / dtype_size(P->dtype) : 1.0);
+    const double all = b * (l.in_bytes_b1 + l.res_bytes_b1) + out_bytes + l.param_bytes;
+    if (l.kind != K_GEMM || layer_launches(l, batch) == 1) {
+        *flops = b * l.flops_b1;
+        *bytes = all;
+        return;
+    }
+    if (launch == 0) {
+        *flops = b * l.flops_b1;
+        *bytes = b * l.in_bytes_b1 + l.param_bytes;
+    } else {
+        *flops = 0;
+        *bytes = b * l.res_bytes_b1 + out_bytes;
+    }
+}
+
+hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, const void* in,
+                         void* out, hipStream_t s, LaunchHook* hook)
+{
+    const void* x = buf_ptr(P, l.in_buf, in, out);
+    void* y = const_cast<void*>(buf_ptr(P, l.out_buf, in, out));
+    const void* res = buf_ptr(P, l.res_buf, in, out);
+    hipError_t e = hipSuccess;
+    switch (l.kind) {
+    case K_GEMM: {
+        const Plan& p = l.plans[batch - 1];
+        ConvGemmArgs a;
+        a.x = x;
+        a.w = l.w;
+        a.scale = l.scale;
+        a.bias = l.bias;
+        a.res = res;
+        a.y = y;
+        a.partial = P->ws;
+        a.N = batch;
+        a.H = l.H; a.W = l.W; a.C = l.C;
+        a.Ho = l.Ho; a.Wo = l.Wo; a.Co = l.Co;
+        a.KH = l.KH; a.KW = l.KW; a.stride = l.gstride; a.pad = l.gpad;
+        a.K = l.K; a.Kpad = l.Kpad;
+        a.M = batch * l.Ho * l.Wo;
+        a.act = l.act;
+        a.total_chunks = p.total_chunks;
+        a.chunks_per_split = p.chunks_per_split;
+        const bool two = l.softmax || p.splits > 1;
+        a.out_mode = two ? 1 : 0;
+        if (hook) hook->before(l, 0, s);
+        e = launch_conv_gemm(P->dtype, p.cfg, l.generic, a, p.splits, s);
+        if (hook) hook->after(l, 0, s);
+        if (e != hipSuccess || !two)
+            return e;
+        if (hook) hook->before(l, 1, s);
+        if (l.softmax)
+            e = launch_splitk_softmax(P->ws, p.splits, a.M, l.Co, l.bias, (float*)y, s);
+        else
+            e = launch_splitk_epilogue(P->dtype, P->ws, p.splits, a.M, l.Co, l.scale, l.bias,
+                                       res, l.act, y, s);
+        if (hook) hook->after(l, 1, s);
+        return e;
+    }
+    case K_DW:
+        if (hook) hook->before(l, 0, s);
+        e = launch_dwconv(P->dtype, x, l.w, l.scale, l.bias, y, batch, l.H, l.W, l.C, l.Ho,
+                          l.Wo, l.k, l.stride, l.pad, l.act, s);
+        if (hook) hook->after(l, 0, s);
+        return e;
+    case K_MAXPOOL:
+        if (hook) hook->before(l, 0, s);
+        e = launch_maxpool(P->dtype, x, y, batch, l.H, l.W, l.C, l.Ho, l.Wo, l.k, l.stride,
+                           l.pad, s);
+        if (hook) hook->after(l, 0, s);
+        return e;
+    default:
+        if (hook) hook->before(l, 0, s);
+        e = launch_gap(P->dtype, x, y, batch, l.H * l.W, l.C, s);
+        if (hook) hook->after(l, 0, s);
+        return e;
+    }
+}
+
+hipError_t enqueue_all(const ppipe_partition* P, int batch, const void* in, void* out,
+                       hipStream_t s, LaunchHook* hook)
+{
+    for (const LayerRT& l : P->L) {
+        hipError_t e = enqueue_layer(P, l, batch, in, out, s, hook);
+        if (e != hipSuccess)
+            return e;
+    }
+    return hipSuccess;
+}
+
+int check_run_args(const ppipe_partition* P, int batch, const void* in, const void* out)
+{
+    if (!P) return fail(PPIPE_E_INVALID, "null partition handle");
+    if (batch < 1 || batch > P->max_batch)
+        return fail(PPIPE_E_INVALID, "batch " + std::to_string(batch) + " outside [1, " +
+                                         std::to_string(P->max_batch) + "]");
+    if (!in || !out) return fail(PPIPE_E_INVALID, "null input or output pointer");
+    if (in == out) return fail(PPIPE_E_INVALID, "input and output must not alias");
+    return PPIPE_OK;
+}
+
+int ensure_device(const ppipe_partition* P)
+{
+    int cur = -1;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipGetDevice", e));
+    if (cur != P->device) {
+        e = hipSetDevice(P->device);
+        if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipSetDevice", e));
+    }
+    return PPIPE_OK;
+}
+
+void release(ppipe_partition* P)
+{
+    for (GraphEntry& g : P->graphs) {
+        (void)hipGraphExecDestroy(g.exec);
+        (void)hipGraphDestroy(g.graph);
+    }
+    P->graphs.clear();
+    for (void* s : P->slots) (void)hipFree(s);
+    P->slots.clear();
+    if (P->ws) (void)hipFree(P->ws);
+    if (P->wblob) (void)hipFree(P->wblob);
+    if (P->cap_stream) (void)hipStreamDestroy(P->cap_stream);
+    P->ws = nullptr;
+    P->wblob = nullptr;
+    P->cap_stream = nullptr;
+}
+
+float median_of(std::vector<float> v)
+{
+    if (v.empty()) return 0.0f;
+    std::sort(v.begin(), v.end());
+    const size_t n = v.size();
+    return n % 2 ? v[n / 2] : 0.5f * (v[n / 2 - 1] + v[n / 2]);
+}
+
+int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int dt)
+{
+    const int n = d->n_layers;
+    const int esz = dtype_size(dt);
+    const int epv = 16 / esz;
+    // ---- shapes of every layer up to end, from the model input ----
+    std::vector<Shape> sh(end);
+    auto shape_of = [&](int i) { return i < 0 ? Shape{d->in_c, d->in_h, d->in_w} : sh[i]; };
+    for (int i = 0; i < end; ++i) {
+        const ppipe_layer_desc& ld = d->layers[i];
+        const std::string who = "layer " + std::to_string(i);
+        if (ld.src < -1 || ld.src >= i)
+            return fail(PPIPE_E_INVALID, who + ": src must name an earlier layer or -1");
+        if (ld.res_src < -1 || ld.res_src >= i)
+            return fail(PPIPE_E_INVALID, who + ": res_src must name an earlier layer or -1");
+        const Shape x = shape_of(ld.src);
+        if (ld.op == PPIPE_OP_CONV || ld.op == PPIPE_OP_MAXPOOL) {
+            if (ld.k < 1 || ld.stride < 1 || ld.pad < 0 || ld.pad >= ld.k)
+                return fail(PPIPE_E_INVALID, who + ": need k >= 1, stride >= 1, 0 <= pad < k");
+            const int ho = (x.h + 2 * ld.pad - ld.k) / ld.stride + 1;
+            const int wo = (x.w + 2 * ld.pad - ld.k) / ld.stride + 1;
+            if (x.h + 2 * ld.pad < ld.k || x.w + 2 * ld.pad < ld.k || ho < 1 || wo < 1)
+                return fail(PPIPE_E_INVALID, who + ": window larger than the padded input");
+            if (ld.op == PPIPE_OP_CONV) {
+                if (ld.c_in != x.c)
+                    return fail(PPIPE_E_INVALID, who + ": c_in " + std::to_string(ld.c_in) +
+                                                     " != producer channels " + std::to_string(x.c));
+                if (ld.c_out < 1 || ld.groups < 1 || ld.c_in % ld.groups || ld.c_out % ld.groups)
+                    return fail(PPIPE_E_INVALID, who + ": bad groups / channel counts");
+                sh[i] = {ld.c_out, ho, wo};
+            } else {
+                sh[i] = {x.c, ho, wo};
+            }
+        } else if (ld.op == PPIPE_OP_AVGPOOL_GLOBAL) {
+            sh[i] = {x.c, 1, 1};
+        } else if (ld.op == PPIPE_OP_FC || ld.op == PPIPE_OP_FC_SOFTMAX) {
+            if ((int64_t)ld.c_in != (int64_t)x.c * x.h * x.w)
+                return fail(PPIPE_E_INVALID, who + ": fc c_in != flattened producer size");
+            if (ld.c_out < 1)
+                return fail(PPIPE_E_INVALID, who + ": fc c_out < 1");
+            sh[i] = {ld.c_out, 1, 1};
+        } else {
+            return fail(PPIPE_E_INVALID, who + ": unknown op " + std::to_string(ld.op));
+        }
+        if (ld.res_src != -1) {
+            const Shape r = shape_of(ld.res_src);
+            if (ld.op != PPIPE_OP_CONV)
+                return fail(PPIPE_E_UNSUPPORTED, who + ": residual add only on CONV layers");
+            if (r.c != sh[i].c || r.h != sh[i].h || r.w != sh[i].w)
+                return fail(PPIPE_E_INVALID, who + ": residual shape differs from output");
+        }
+    }
+    // ---- the split: one feature map enters, one leaves ----
+    for (int i = begin; i < end; ++i) {
+        const ppipe_layer_desc& ld = d->layers[i];
+        const int refs[2] = {ld.src, ld.res_src};
+        for (int t = 0; t < 2; ++t) {
+            const int r = refs[t];
+            if (t == 1 && r == -1) continue;   // no residual
+            if (r >= begin || r == begin - 1) continue;
+            return fail(PPIPE_E_SPLIT, "layer " + std::to_string(i) + " reads layer " +
+                                           std::to_string(r) + ", produced before the partition "
+                                           "input (layer " + std::to_string(begin - 1) + ")");
+        }
+        if (ld.op == PPIPE_OP_FC_SOFTMAX && i != end - 1)
+            return fail(PPIPE_E_UNSUPPORTED, "layer " + std::to_string(i) +
+                                                 ": FC_SOFTMAX must be the range's last layer");
+    }
+    for (int j = end; j < n; ++j) {
+        const ppipe_layer_desc& ld = d->layers[j];
+        const int refs[2] = {ld.src, ld.res_src};
+        for (int r : refs)
+            if (r >= begin && r < end - 1)
+                return fail(PPIPE_E_SPLIT, "layer " + std::to_string(j) + " (after the range) "
+                                           "reads layer " + std::to_string(r) + " inside it");
+    }
+
+    // ---- per-layer runtime records and kernel constraints ----
+    P->L.resize(end - begin);
+    for (int i = begin; i < end; ++i) {
+        const ppipe_layer_desc& ld = d->layers[i];
+        LayerRT& l = P->L[i - begin];
+        const Shape x = shape_of(ld.src), o = sh[i];
+        const std::string who = "layer " + std::to_string(i);
+        l.index = i; l.op = ld.op; l.src = ld.src; l.res_src = ld.res_src; l.act = ld.act;
+        l.k = ld.k; l.stride = ld.stride; l.pad = ld.pad; l.groups = ld.groups;
+        l.H = x.h; l.W = x.w; l.C = x.c; l.Ho = o.h; l.Wo = o.w; l.Co = o.c;
+        if (ld.act < PPIPE_ACT_NONE || ld.act > PPIPE_ACT_RELU6)
+            return fail(PPIPE_E_INVALID, who + ": unknown activation");
+        l.out_bytes_b1 = (int64_t)o.c * o.h * o.w * esz;
+        l.in_bytes_b1 = (double)x.c * x.h * x.w * esz;
+        l.res_bytes_b1 = ld.res_src >= 0 ? (double)l.out_bytes_b1 : 0.0;
+        if (ld.op == PPIPE_OP_CONV && ld.groups > 1) {
+            if (!(ld.groups == ld.c_in && ld.c_in == ld.c_out))
+                return fail(PPIPE_E_UNSUPPORTED, who + ": grouped conv other than depthwise");
+            if (ld.k != 3 || x.c % epv || ld.res_src >= 0)
+                return fail(PPIPE_E_UNSUPPORTED, who + ": depthwise kernel needs k = 3, C % " +
+                                                     std::to_string(epv) + " == 0, no residual");
+            if (!ld.weight)
+                return fail(PPIPE_E_INVALID, who + ": missing weight");
+            l.kind = K_DW;
+            l.flops_b1 = 2.0 * o.c * o.h * o.w * ld.k * ld.k;
+            l.param_bytes = (double)ld.k * ld.k * o.c * esz + 8.0 * o.c;
+        } else if (ld.op == PPIPE_OP_CONV || ld.op == PPIPE_OP_FC ||
+                   ld.op == PPIPE_OP_FC_SOFTMAX) {
+            l.kind = K_GEMM;
+            l.softmax = ld.op == PPIPE_OP_FC_SOFTMAX;
+            if (ld.op == PPIPE_OP_CONV) {
+                l.KH = l.KW = ld.k;
+                l.gstride = ld.stride;
+                l.gpad = ld.pad;
+            } else {   // fc = valid H x W convolution producing 1 x 1
+                l.KH = x.h;
+                l.KW = x.w;
+                l.gstride = 1;
+                l.gpad = 0;
+                if (l.softmax && o.c > SOFTMAX_MAX_O)
+                    return fail(PPIPE_E_UNSUPPORTED, who + ": softmax over more than " +
+                                                         std::to_string(SOFTMAX_MAX_O) + " classes");
+            }
+            if (o.c % 4)
+                return fail(PPIPE_E_UNSUPPORTED, who + ": output channels must be a multiple of 4");
+            l.K = l.KH * l.KW * x.c;
+            l.Kpad = (l.K + 63) / 64 * 64;
+            const int bk_min = gemm_bk(GEMM_128x128, dt);   // every config uses the same BK
+            l.generic = !(x.c % epv == 0 && (l.KH * l.KW == 1 || x.c % bk_min == 0));
+            if (l.generic && l.Kpad > GEMM_KTAB_MAX)
+                return fail(PPIPE_E_UNSUPPORTED, who + ": reduction length " +
+                                                     std::to_string(l.K) + " with C = " +
+                                                     std::to_string(x.c) + " is not supported");
+            if (!ld.weight)
+                return fail(PPIPE_E_INVALID, who + ": missing weight");
+            l.flops_b1 = 2.0 * o.c * o.h * o.w * (double)l.K;
+            l.param_bytes = (double)o.c * l.K * esz + 8.0 * o.c;
+        } else if (ld.op == PPIPE_OP_MAXPOOL) {
+            if (x.c % epv)
+                return fail(PPIPE_E_UNSUPPORTED, who + ": maxpool needs C % " +
+                                                     std::to_string(epv) + " == 0");
+            l.kind = K_MAXPOOL;
+            l.flops_b1 = 0;
+        } else {
+            if (x.c % epv)
+                return fail(PPIPE_E_UNSUPPORTED, who + ": avgpool needs C % " +
+                                                     std::to_string(epv) + " == 0");
+            l.kind = K_GAP;
+            l.flops_b1 = (double)x.c * x.h * x.w;
+        }
+        if (ld.op == PPIPE_OP_CONV && ld.bn_gamma &&
+            !(ld.bn_beta && ld.bn_mean && ld.bn_var))
+            return fail(PPIPE_E_INVALID, who + ": batch norm needs gamma, beta, mean and var");
+    }
+
+    // ---- weights, folded scale / shift: one device blob ----
+    auto align = [](size_t v) { return (v + 255) / 256 * 256; };
+    size_t total = 0;
+    for (LayerRT& l : P->L) {
+        if (l.kind == K_GEMM) {
+            l.w_off = total; total = align(total + (size_t)l.Co * l.Kpad * esz);
+        } else if (l.kind == K_DW) {
+            l.w_off = total; total = align(total + (size_t)l.k * l.k * l.Co * esz);
+        } else {
+            continue;
+        }
+        l.scale_off = total; total = align(total + (size_t)l.Co * 4);
+        l.bias_off = total; total = align(total + (size_t)l.Co * 4);
+    }
+    std::vector<uint8_t> blob(std::max<size_t>(total, 256), 0);
+    for (LayerRT& l : P->L) {
+        if (l.kind != K_GEMM && l.kind != K_DW) continue;
+        const ppipe_layer_desc& ld = d->layers[l.index];
+        if (l.kind == K_GEMM) {
+            if (l.op == PPIPE_OP_CONV) {
+                // OIHW [co][ci][kh][kw] -> [co][(kh * KW + kw) * C + ci]
+                for (int co = 0; co < l.Co; ++co)
+                    for (int ci = 0; ci < l.C; ++ci)
+                        for (int kh = 0; kh < l.KH; ++kh)
+                            for (int kw = 0; kw < l.KW; ++kw)
+                                put_elem(blob, l.w_off, dt,
+                                         (size_t)co * l.Kpad + (size_t)(kh * l.KW + kw) * l.C + ci,
+                                         ld.weight[(((size_t)co * l.C + ci) * l.KH + kh) * l.KW + kw]);
+            } else {
+                // [o][c * H * W + h * W + w] -> [o][(h * W + w) * C + c]
+                for (int co = 0; co < l.Co; ++co)
+                    for (int c = 0; c < l.C; ++c)
+                        for (int h = 0; h < l.KH; ++h)
+                            for (int w = 0; w < l.KW; ++w)
+                                put_elem(blob, l.w_off, dt,
+                                         (size_t)co * l.Kpad + (size_t)(h * l.KW + w) * l.C + c,
+                                         ld.weight[(size_t)co * l.K + ((size_t)c * l.KH + h) * l.KW + w]);
+            }
+        } else {
+            // depthwise OIHW [c][1][kh][kw] -> [kh][kw][c]
+            for (int c = 0; c < l.Co; ++c)
+                for (int kh = 0; kh < l.k; ++kh)
+                    for (int kw = 0; kw < l.k; ++kw)
+                        put_elem(blob, l.w_off, dt, (size_t)(kh * l.k + kw) * l.Co + c,
+                                 ld.weight[((size_t)c * l.k + kh) * l.k + kw]);
+        }
+        float* sc = (float*)&blob[l.scale_off];
+        float* bi = (float*)&blob[l.bias_off];
+        const bool bn = l.op == PPIPE_OP_CONV && ld.bn_gamma;
+        const double eps = ld.bn_eps > 0.0f ? (double)ld.bn_eps : 1e-5;
+        for (int c = 0; c < l.Co; ++c) {
+            const double b0 = ld.bias ? (double)ld.bias[c] : 0.0;
+            if (bn) {
+                // (acc + b0 - mean) / sqrt(var + eps) * gamma + beta = acc * s + t
+                const double s = (double)ld.bn_gamma[c] / std::sqrt((double)ld.bn_var[c] + eps);
+                sc[c] = (float)s;
+                bi[c] = (float)((double)ld.bn_beta[c] + (b0 - (double)ld.bn_mean[c]) * s);
+            } else {
+                sc[c] = 1.0f;
+                bi[c] = (float)b0;
+            }
+        }
+    }
+    P->host_blob.swap(blob);
+
+    // ---- activation buffers by liveness ----
+    std::vector<int> last_use(end - begin, -1);
+    for (int i = begin; i < end; ++i) {
+        const ppipe_layer_desc& ld = d->layers[i];
+        for (int r : {ld.src, ld.res_src})
+            if (r >= begin) last_use[r - begin] = std::max(last_use[r - begin], i);
+    }
+    std::vector<int> slot_busy_until;
+    for (int i = begin; i < end; ++i) {
+        LayerRT& l = P->L[i - begin];
+        const ppipe_layer_desc& ld = d->layers[i];
+        l.in_buf = ld.src >= begin ? P->L[ld.src - begin].out_buf : BUF_IN;
+        l.res_buf = ld.res_src == -1 ? BUF_NONE
+                    : (ld.res_src >= begin ? P->L[ld.res_src - begin].out_buf : BUF_IN);
+        if (i == end - 1) {
+            l.out_buf = BUF_OUT;
+            break;
+        }
+        const size_t need = (size_t)P->max_batch * (size_t)l.out_bytes_b1;
+        int slot = -1;
+        for (size_t s = 0; s < slot_busy_until.size(); ++s)
+            if (slot_busy_until[s] < i) {
+                // prefer a free slot that is already large enough
+                if (slot < 0 || (P->slot_bytes[s] >= need && P->slot_bytes[slot] < need))
+                    slot = (int)s;
+            }
+        if (slot < 0) {
+            slot = (int)slot_busy_until.size();
+            slot_busy_until.push_back(-1);
+            P->slot_bytes.push_back(0);
+        }
+        slot_busy_until[slot] = std::max(last_use[i - begin], i);
+        P->slot_bytes[slot] = std::max(P->slot_bytes[slot], need);
+        l.out_buf = slot;
+    }
+
+    // ---- kernel plans for every batch, split-K workspace ----
+    size_t ws = 0;
+    for (LayerRT& l : P->L) {
+        if (l.kind != K_GEMM) continue;
+        l.plans.resize(P->max_batch);
+        for (int b = 1; b <= P->max_batch; ++b) {
+            const int M = b * l.Ho * l.Wo;
+            Plan p = choose_plan(M, l.Co, l.K, dt);
+            l.plans[b - 1] = p;
+            if (p.splits > 1 || l.softmax)
+                ws = std::max(ws, (size_t)p.splits * M * l.Co * sizeof(float));
+        }
+    }
+    P->ws_bytes = ws;
+    const LayerRT& last = P->L.back();
+    P->in = shape_of(d->layers[begin].src);
+    P->out = {last.Co, last.Ho, last.Wo};
+    P->out_dtype = last.softmax ? DT_F32 : dt;
+    return PPIPE_OK;
+}
+
+// Device side of create: upload weights, allocate buffers, make the capture stream.
+int allocate(ppipe_partition* P)
+{
+    hipError_t e = hipGetDevice(&P->device);
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipGetDevice", e));
+    e = hipMalloc(&P->wblob, P->host_blob.size());
+    if (e != hipSuccess) return fail(PPIPE_E_NOMEM, hip_msg("hipMalloc(weights)", e));
+    P->wbytes = P->host_blob.size();
+    e = hipMemcpy(P->wblob, P->host_blob.data(), P->host_blob.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipMemcpy(weights)", e));
+    std::vector<uint8_t>().swap(P->host_blob);
+    for (LayerRT& l : P->L) {
+        if (l.kind != K_GEMM && l.kind != K_DW) continue;
+        l.w = (uint8_t*)P->wblob + l.w_off;
+        l.scale = (float*)((uint8_t*)P->wblob + l.scale_off);
+        l.bias = (float*)((uint8_t*)P->wblob + l.bias_off);
+    }
+    P->slots.assign(P->slot_bytes.size(), nullptr);
+    for (size_t s = 0; s < P->slots.size(); ++s) {
+        e = hipMalloc(&P->slots[s], P->slot_bytes[s]);
+        if (e != hipSuccess) return fail(PPIPE_E_NOMEM, hip_msg("hipMalloc(activations)", e));
+    }
+    if (P->ws_bytes) {
+        e = hipMalloc((void**)&P->ws, P->ws_bytes);
+        if (e != hipSuccess) return fail(PPIPE_E_NOMEM, hip_msg("hipMalloc(split-K)", e));
+    }
+    e = hipStreamCreateWithFlags(&P->cap_stream, hipStreamNonBlocking);
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipStreamCreate", e));
+    return PPIPE_OK;
+}
+
+// Event hook for per-launch timing.
+struct EventHook : LaunchHook {
+    std::vector<hipEvent_t> ev;   // 2 per launch
+    size_t next = 0;
+    hipError_t err = hipSuccess;
+    void before(const LayerRT&, int, hipStream_t s) override
+    {
+        if (err == hipSuccess) err = hipEventRecord(ev[next++], s);
+    }
+    void after(const LayerRT&, int, hipStream_t s) override
+    {
+        if (err == hipSuccess) err = hipEventRecord(ev[next++], s);
+    }
+};
+
+struct ProfileBuffers {
+    void* in = nullptr;
+    void* out = nullptr;
+    hipStream_t s = nullptr;
+    ~ProfileBuffers()
+    {
+        if (s) (void)hipStreamSynchronize(s);
+        if (in) (void)hipFree(in);
+        if (out) (void)hipFree(out);
+        if (s) (void)hipStreamDestroy(s);
+    }
+};
+
+int setup_profile(ppipe_partition* P, ProfileBuffers& pb)
+{
+    const size_t in_b = (size_t)P->max_batch * P->in.c * P->in.h * P->in.w * dtype_size(P->dtype);
+    const size_t out_b = (size_t)P->max_batch * P->out.c * P->out.h * P->out.w *
+                         dtype_size(P->out_dtype);
+    hipError_t e = hipStreamCreateWithFlags(&pb.s, hipStreamNonBlocking);
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipStreamCreate", e));
+    if ((e = hipMalloc(&pb.in, in_b)) != hipSuccess ||
+        (e = hipMalloc(&pb.out, out_b)) != hipSuccess)
+        return fail(PPIPE_E_NOMEM, hip_msg("hipMalloc(profile buffers)", e));
+    e = launch_fill_uniform(P->dtype, pb.in, in_b / dtype_size(P->dtype), 12345u, pb.s);
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("fill", e));
+    return PPIPE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ppipe_last_error(void) { return g_err.c_str(); }
+
+int32_t ppipe_last_status(void) { return g_status; }
+
+ppipe_partition* ppipe_partition_create(const ppipe_model_desc* desc, int32_t layer_begin,
+                                        int32_t layer_end, int32_t dtype)
+{
+    g_err.clear();
+    g_status = 0;
+    if (!desc || !desc->layers || desc->n_layers < 1) {
+        fail(PPIPE_E_INVALID, "model description is empty");
+        return nullptr;
+    }
+    if (dtype < PPIPE_F32 || dtype > PPIPE_BF16) {
+        fail(PPIPE_E_INVALID, "unknown dtype " + std::to_string(dtype));
+        return nullptr;
+    }
+    if (layer_begin < 0 || layer_end > desc->n_layers || layer_begin >= layer_end) {
+        fail(PPIPE_E_INVALID, "layer range [" + std::to_string(layer_begin) + ", " +
+                                  std::to_string(layer_end) + ") is empty or outside the model");
+        return nullptr;
+    }
+    if (desc->in_c < 1 || desc->in_h < 1 || desc->in_w < 1) {
+        fail(PPIPE_E_INVALID, "model input shape must be positive");
+        return nullptr;
+    }
+    ppipe_partition* P = new ppipe_partition();
+    P->begin = layer_begin;
+    P->end = layer_end;
+    P->dtype = dtype;
+    P->max_batch = desc->max_batch > 0 ? desc->max_batch : 64;
+    // host-side validation and packing first: a bad description fails
+    // without touching the device
+    if (build(P, desc, layer_begin, layer_end, dtype) != PPIPE_OK || allocate(P) != PPIPE_OK) {
+        std::string msg = g_err;
+        const int st = g_status;
+        release(P);
+        delete P;
+        g_err = msg;
+        g_status = st;
+        return nullptr;
+    }
+    return P;
+}
+
+void ppipe_partition_destroy(ppipe_partition* h)
+{
+    if (!h) return;
+    ensure_device(h);
+    (void)hipDeviceSynchronize();
+    release(h);
+    delete h;
+}
+
+int ppipe_partition_run(ppipe_partition* h, int32_t batch, const void* in, void* out,
+                        void* stream)
+{
+    int rc = check_run_args(h, batch, in, out);
+    if (rc != PPIPE_OK) return rc;
+    if ((rc = ensure_device(h)) != PPIPE_OK) return rc;
+    hipStream_t s = (hipStream_t)stream;
+    for (const GraphEntry& g : h->graphs) {
+        if (g.batch == batch && g.in == in && g.out == out) {
+            hipError_t e = hipGraphLaunch(g.exec, s);
+            if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipGraphLaunch", e));
+            return PPIPE_OK;
+        }
+    }
+    hipError_t e = enqueue_all(h, batch, in, out, s, nullptr);
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("kernel launch", e));
+    return PPIPE_OK;
+}
+
+int ppipe_partition_capture(ppipe_partition* h, int32_t batch, const void* in, void* out)
+{
+    int rc = check_run_args(h, batch, in, out);
+    if (rc != PPIPE_OK) return rc;
+    if ((rc = ensure_device(h)) != PPIPE_OK) return rc;
+    for (const GraphEntry& g : h->graphs)
+        if (g.batch == batch && g.in == in && g.out == out) return PPIPE_OK;
+    hipError_t e = hipStreamBeginCapture(h->cap_stream, hipStreamCaptureModeThreadLocal);
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipStreamBeginCapture", e));
+    hipError_t le = enqueue_all(h, batch, in, out, h->cap_stream, nullptr);
+    hipGraph_t g = nullptr;
+    e = hipStreamEndCapture(h->cap_stream, &g);
+    if (le != hipSuccess || e != hipSuccess) {
+        if (g) (void)hipGraphDestroy(g);
+        return fail(PPIPE_E_HIP, hip_msg("graph capture", le != hipSuccess ? le : e));
+    }
+    hipGraphExec_t x = nullptr;
+    e = hipGraphInstantiate(&x, g, nullptr, nullptr, 0);
+    if (e != hipSuccess) {
+        (void)hipGraphDestroy(g);
+        return fail(PPIPE_E_HIP, hip_msg("hipGraphInstantiate", e));
+    }
+    h->graphs.push_back({batch, in, out, g, x});
+    return PPIPE_OK;
+}
+
+int ppipe_profile_layers(ppipe_partition* h, const int32_t* batch_sizes, int32_t n_batches,
+                         int32_t warmup, int32_t reps, float* out_us, float* out_partition_us)
+{
+    if (!h) return fail(PPIPE_E_INVALID, "null partition handle");
+    if (!batch_sizes || n_batches < 1 || warmup < 0 || reps < 1)
+        return fail(PPIPE_E_INVALID, "need batch sizes, warmup >= 0 and reps >= 1");
+    for (int j = 0; j < n_batches; ++j)
+        if (batch_sizes[j] < 1 || batch_sizes[j] > h->max_batch)
+            return fail(PPIPE_E_INVALID, "batch size outside [1, max_batch]");
+    int rc = ensure_device(h);
+    if (rc != PPIPE_OK) return rc;
+    ProfileBuffers pb;
+    if ((rc = setup_profile(h, pb)) != PPIPE_OK) return rc;
+    const int nl = (int)h->L.size();
+    std::vector<hipEvent_t> ev(nl + 1);
+    for (auto& x : ev) {
+        hipError_t e = hipEventCreate(&x);
+        if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipEventCreate", e));
+    }
+    struct EvGuard {
+        std::vector<hipEvent_t>& v;
+        ~EvGuard() { for (auto x : v) if (x) (void)hipEventDestroy(x); }
+    } guard{ev};
+    for (int j = 0; j < n_batches; ++j) {
+        const int b = batch_sizes[j];
+        hipError_t e = hipSuccess;
+        for (int w = 0; w < warmup && e == hipSuccess; ++w)
+            e = enqueue_all(h, b, pb.in, pb.out, pb.s, nullptr);
+        if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("kernel launch", e));
+        std::vector<std::vector<float>> per(nl);
+        std::vector<float> whole;
+        for (int r = 0; r < reps; ++r) {
+            e = hipEventRecord(ev[0], pb.s);
+            for (int i = 0; i < nl && e == hipSuccess; ++i) {
+                e = enqueue_layer(h, h->L[i], b, pb.in, pb.out, pb.s, nullptr);
+                if (e == hipSuccess) e = hipEventRecord(ev[i + 1], pb.s);
+            }
+            if (e == hipSuccess) e = hipEventSynchronize(ev[nl]);
+            if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("profile run", e));
+            for (int i = 0; i < nl; ++i) {
+                float ms = 0;
+                (void)hipEventElapsedTime(&ms, ev[i], ev[i + 1]);
+                per[i].push_back(ms * 1000.0f);
+            }
+        }
+        for (int r = 0; r < reps; ++r) {
+            e = hipEventRecord(ev[0], pb.s);
+            if (e == hipSuccess) e = enqueue_all(h, b, pb.in, pb.out, pb.s, nullptr);
+            if (e == hipSuccess) e = hipEventRecord(ev[1], pb.s);
+            if (e == hipSuccess) e = hipEventSynchronize(ev[1]);
+            if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("profile run", e));
+            float ms = 0;
+            (void)hipEventElapsedTime(&ms, ev[0], ev[1]);
+            whole.push_back(ms * 1000.0f);
+        }
+        if (out_us)
+            for (int i = 0; i < nl; ++i) out_us[(size_t)i * n_batches + j] = median_of(per[i]);
+        if (out_partition_us) out_partition_us[j] = median_of(whole);
+    }
+    return PPIPE_OK;
+}
+
+int ppipe_profile_kernels(ppipe_partition* h, int32_t batch, int32_t warmup, int32_t reps,
+                          ppipe_kernel_record* records, int32_t capacity, int32_t* count)
+{
+    if (!h) return fail(PPIPE_E_INVALID, "null partition handle");
+    if (batch < 1 || batch > h->max_batch || warmup < 0 || reps < 1 || !count)
+        return fail(PPIPE_E_INVALID, "bad batch, warmup, reps or count pointer");
+    int rc = ensure_device(h);
+    if (rc != PPIPE_OK) return rc;
+    int nlaunch = 0;
+    for (const LayerRT& l : h->L) nlaunch += layer_launches(l, batch);
+    *count = nlaunch;
+    ProfileBuffers pb;
+    if ((rc = setup_profile(h, pb)) != PPIPE_OK) return rc;
+    EventHook hook;
+    hook.ev.resize(2 * (size_t)nlaunch);
+    for (auto& x : hook.ev) {
+        hipError_t e = hipEventCreate(&x);
+        if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipEventCreate", e));
+    }
+    struct EvGuard {
+        std::vector<hipEvent_t>& v;
+        ~EvGuard() { for (auto x : v) if (x) (void)hipEventDestroy(x); }
+    } guard{hook.ev};
+    hipError_t e = hipSuccess;
+    for (int w = 0; w < warmup && e == hipSuccess; ++w)
+        e = enqueue_all(h, batch, pb.in, pb.out, pb.s, nullptr);
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("kernel launch", e));
+    std::vector<std::vector<float>> t(nlaunch);
+    for (int r = 0; r < reps; ++r) {
+        hook.next = 0;
+        e = enqueue_all(h, batch, pb.in, pb.out, pb.s, &hook);
+        if (e == hipSuccess) e = hook.err;
+        if (e == hipSuccess) e = hipEventSynchronize(hook.ev.back());
+        if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("profile run", e));
+        for (int k = 0; k < nlaunch; ++k) {
+            float ms = 0;
+            (void)hipEventElapsedTime(&ms, hook.ev[2 * k], hook.ev[2 * k + 1]);
+            t[k].push_back(ms * 1000.0f);
+        }
+    }
+    int k = 0;
+    for (const LayerRT& l : h->L) {
+        for (int j = 0; j < layer_launches(l, batch); ++j, ++k) {
+            if (!records || k >= capacity) continue;
+            ppipe_kernel_record& rec = records[k];
+            std::memset(&rec, 0, sizeof(rec));
+            rec.layer = l.index;
+            rec.launch = j;
+            std::snprintf(rec.kernel, sizeof(rec.kernel), "%s",
+                          launch_name(h, l, batch, j).c_str());
+            launch_work(h, l, batch, j, &rec.flops, &rec.bytes);
+            double sum = 0;
+            float mn = t[k].empty() ? 0.f : t[k][0];
+            for (float v : t[k]) { sum += v; mn = std::min(mn, v); }
+            rec.mean_us = (float)(sum / std::max<size_t>(1, t[k].size()));
+            rec.median_us = median_of(t[k]);
+            rec.min_us = mn;
+        }
+    }
+    return PPIPE_OK;
+}
+
+int ppipe_partition_info(const ppipe_partition* h, ppipe_partition_info_t* info)
+{
+    if (!h || !info) return fail(PPIPE_E_INVALID, "null argument");
+    std::memset(info, 0, sizeof(*info));
+    info->layer_begin = h->begin;
+    info->layer_end = h->end;
+    info->dtype = h->dtype;
+    info->max_batch = h->max_batch;
+    info->in_c = h->in.c; info->in_h = h->in.h; info->in_w = h->in.w;
+    info->out_c = h->out.c; info->out_h = h->out.h; info->out_w = h->out.w;
+    info->out_dtype = h->out_dtype;
+    info->in_bytes_per_image = (int64_t)h->in.c * h->in.h * h->in.w * dtype_size(h->dtype);
+    info->out_bytes_per_image = (int64_t)h->out.c * h->out.h * h->out.w * dtype_size(h->out_dtype);
+    info->weight_bytes = (int64_t)h->wbytes;
+    size_t ws = h->ws_bytes;
+    for (size_t b : h->slot_bytes) ws += b;
+    info->workspace_bytes = (int64_t)ws;
+    return PPIPE_OK;
+}
+
+int ppipe_layer_info(const ppipe_partition* h, int32_t index, int32_t batch,
+                     ppipe_layer_info_t* info)
+{
+    if (!h || !info) return fail(PPIPE_E_INVALID, "null argument");
+    if (index < h->begin || index >= h->end)
+        return fail(PPIPE_E_INVALID, "layer index outside the partition");
+    if (batch < 1 || batch > h->max_batch)
+        return fail(PPIPE_E_INVALID, "batch outside [1, max_batch]");
+    const LayerRT& l = h->L[index - h->begin];
+    std::memset(info, 0, sizeof(*info));
+    info->index = l.index;
+    info->op = l.op;
+    info->out_c = l.Co; info->out_h = l.Ho; info->out_w = l.Wo;
+    info->kernel_count = layer_launches(l, batch);
+    info->out_bytes_b1 = l.softmax ? (int64_t)l.Co * 4 : l.out_bytes_b1;
+    info->flops_b1 = l.flops_b1;
+    info->act_bytes_b1 = l.in_bytes_b1 + l.res_bytes_b1 + (double)info->out_bytes_b1;
+    info->param_bytes = l.param_bytes;
+    std::string k = launch_name(h, l, batch, 0);
+    if (l.kind == K_GEMM) {
+        const Plan& p = l.plans[batch - 1];
+        k += " splits=" + std::to_string(p.splits);
+    }
+    std::snprintf(info->kernel, sizeof(info->kernel), "%s", k.c_str());
+    return PPIPE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,146 @@
+"""Kernel parity: each kernel family, tile configuration, split-K path and
+dtype against the CPU oracle on small seeded layers that span several tiles
+and ragged tails.  Runs through the C ABI on an MI355X."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+from workloads.zoo import Layer, Model
+
+from gpu_util import gpu_forward, rel_inf, argmax_rows
+
+pytestmark = pytest.mark.gpu
+
+# one rounding to the storage dtype on each side plus fp32-vs-fp64 sums
+LAYER_TOL = {"f32": 1e-5, "f16": 2.0 ** -9, "bf16": 2.0 ** -7}
+DTYPES = ["f32", "f16", "bf16"]
+
+
+def make(in_chw, specs):
+    m = Model("t", *in_chw)
+    for s in specs:
+        m.add(**s)
+    return m
+
+
+def check(m, dtype, batch, begin=0, end=None, seed=0, kind="normal", in_chw=None, tol=None,
+          exact=False):
+    from paper_2507_18748_amd import Partition
+    end = len(m.layers) if end is None else end
+    P = W.model_params(m, seed, dtype, begin, end)
+    in_chw = in_chw or (m.in_c, m.in_h, m.in_w)
+    x = W.partition_input(in_chw, batch, seed, dtype, kind)
+    print(f"[layer-parity] {[L.name for L in m.layers[begin:end]]} dtype={dtype} batch={batch}",
+          flush=True)
+    ref = oracle.forward(m.layers, P, begin, end, x, dtype)
+    with Partition(m.layers, P, (m.in_c, m.in_h, m.in_w), begin, end, dtype, max_batch=batch) as part:
+        got = gpu_forward(part, x)
+    got = got.reshape(ref.shape)
+    if exact:
+        np.testing.assert_array_equal(got, ref)
+        return 0.0
+    e = rel_inf(got, ref)
+    assert e <= (tol or LAYER_TOL[dtype]), f"rel_inf {e:.3e}"
+    if m.layers[end - 1].op == "fc_softmax":
+        assert (argmax_rows(got) == argmax_rows(ref)).all()
+    return e
+
+
+def conv(name, src, ci, co, k=1, s=1, p=0, g=1, act="relu", res=-1, bn=True, bias=False):
+    return dict(name=name, op="conv", src=src, c_in=ci, c_out=co, k=k, stride=s, pad=p,
+                groups=g, act=act, res_src=res, bn=bn, bias=bias)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_conv3x3_split_k(dtype):
+    # M = 2*15*15 = 450 (ragged), Co = 128: 64x64 tiles with split-K
+    check(make((64, 15, 15), [conv("c", -1, 64, 128, 3, 1, 1)]), dtype, 2)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_conv3x3_stride2_ragged(dtype):
+    check(make((32, 17, 17), [conv("c", -1, 32, 64, 3, 2, 1)]), dtype, 3)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_conv1x1_k_tail(dtype):
+    # C = 24 is not a multiple of the K stage: masked tail; Co = 40 ragged tile
+    check(make((24, 10, 10), [conv("c", -1, 24, 40, act="none")]), dtype, 2)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_conv1x1_stride2_downsample(dtype):
+    check(make((64, 14, 14), [conv("c", -1, 64, 128, 1, 2, 0, act="none")]), dtype, 2)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_residual_from_partition_input(dtype):
+    m = make((16, 9, 9), [conv("c0", -1, 16, 32, 3, 1, 1),
+                          conv("c1", 0, 32, 16, 1),
+                          conv("c2", 1, 16, 32, 3, 1, 1, res=0)])
+    check(m, dtype, 3, begin=1, end=3, in_chw=(32, 9, 9))
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_stem7x7_gather(dtype):
+    check(make((3, 32, 32), [conv("stem", -1, 3, 64, 7, 2, 3)]), dtype, 2, kind="image")
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_stem3x3_relu6_gather(dtype):
+    check(make((3, 33, 33), [conv("stem", -1, 3, 32, 3, 2, 1, act="relu6")]), dtype, 2,
+          kind="image")
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("stride", [1, 2])
+def test_depthwise3x3(dtype, stride):
+    check(make((96, 13, 13), [conv("dw", -1, 96, 96, 3, stride, 1, g=96, act="relu6")]),
+          dtype, 2)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("k,s,p,hw", [(3, 2, 1, 15), (2, 2, 0, 12), (3, 2, 1, 112)])
+def test_maxpool_bit_exact(dtype, k, s, p, hw):
+    m = make((64, hw, hw), [dict(name="pool", op="maxpool", src=-1, c_in=64, c_out=64, k=k,
+                                 stride=s, pad=p)])
+    check(m, dtype, 2, exact=True)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_global_avgpool(dtype):
+    check(make((256, 7, 7), [dict(name="gap", op="gap", src=-1, c_in=256, c_out=256)]),
+          dtype, 3, kind="relu_normal")
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_gap_fc_softmax(dtype):
+    m = make((512, 7, 7), [dict(name="gap", op="gap", src=-1, c_in=512, c_out=512),
+                           dict(name="fc", op="fc_softmax", src=0, c_in=512, c_out=1000,
+                                bias=True)])
+    check(m, dtype, 5, kind="relu_normal", tol={"f32": 1e-5, "f16": 1e-2, "bf16": 2e-2}[dtype])
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_fc_on_feature_map(dtype):
+    # FC over a 7x7x64 map flattened in (c, h, w) order, then FC + softmax
+    m = make((64, 7, 7), [dict(name="fc6", op="fc", src=-1, c_in=64 * 49, c_out=256,
+                               act="relu", bias=True),
+                          dict(name="fc8", op="fc_softmax", src=0, c_in=256, c_out=100,
+                               bias=True)])
+    check(m, dtype, 3, kind="relu_normal", tol={"f32": 1e-5, "f16": 1e-2, "bf16": 2e-2}[dtype])
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_conv_large_tiles(dtype):
+    # M = 8*64*64 = 32768, Co = 128: the 128x128 tile configuration
+    check(make((32, 64, 64), [conv("c", -1, 32, 128, 3, 1, 1)]), dtype, 8)
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_fc_large_k_small_batch(dtype):
+    # M = batch = 1: 64x16 tiles, deep split-K over K = 4096
+    m = make((4096, 1, 1), [dict(name="fc", op="fc", src=-1, c_in=4096, c_out=1000,
+                                 act="relu", bias=True)])
+    check(m, dtype, 1)

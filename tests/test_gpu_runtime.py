@@ -1,0 +1,73 @@
+"""Runtime behaviour through the C ABI: repeatability, graph replay,
+batch-size sweep on one handle, profiling tables and error paths."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as W
+
+from gpu_util import gpu_forward, rel_inf, upload_nhwc, empty_out
+
+pytestmark = pytest.mark.gpu
+
+
+def _small():
+    wl = W.workload("resnet50_layer4_head")
+    m = wl.build_model()
+    return wl, m, wl.params(m)
+
+
+def test_bitwise_repeatable_and_graph_replay_matches_eager():
+    import torch
+    from paper_2507_18748_amd import Partition
+    wl, m, P = _small()
+    x = wl.input(8)
+    with Partition(m.layers, P, (3, 224, 224), wl.begin, wl.end, wl.dtype, max_batch=8) as part:
+        a = gpu_forward(part, x)
+        b = gpu_forward(part, x)
+        np.testing.assert_array_equal(a, b)
+        xd = upload_nhwc(x, wl.dtype)
+        out = empty_out(part, 8)
+        part.capture(8, xd.data_ptr(), out.data_ptr())
+        s = torch.cuda.current_stream().cuda_stream
+        for _ in range(4):
+            out.zero_()
+            part.run(8, xd.data_ptr(), out.data_ptr(), s)
+            torch.cuda.synchronize()
+            _ = (xd.float() * 2).sum().item()      # unrelated eager work between replays
+            got = out.float().cpu().numpy().transpose(0, 3, 1, 2)
+            np.testing.assert_array_equal(got, a)
+
+
+def test_batch_sweep_on_one_handle():
+    from paper_2507_18748_amd import Partition
+    wl, m, P = _small()
+    x = wl.input(16)
+    ref0 = oracle.forward(m.layers, P, wl.begin, wl.end, x[:1], wl.dtype)
+    with Partition(m.layers, P, (3, 224, 224), wl.begin, wl.end, wl.dtype, max_batch=16) as part:
+        for b in (1, 2, 3, 5, 8, 13, 16):
+            got = gpu_forward(part, x[:b])
+            assert rel_inf(got[:1].reshape(ref0.shape), ref0) <= 2e-2
+        from paper_2507_18748_amd import PpipeError
+        with pytest.raises(PpipeError):
+            part.run(17, 1, 2, 0)
+        with pytest.raises(PpipeError):
+            part.run(0, 1, 2, 0)
+
+
+def test_profile_tables():
+    from paper_2507_18748_amd import Partition
+    wl, m, P = _small()
+    with Partition(m.layers, P, (3, 224, 224), wl.begin, wl.end, wl.dtype, max_batch=8) as part:
+        table, whole = part.profile_layers([1, 2, 8], warmup=3, reps=10)
+        assert table.shape == (12, 3)
+        assert np.isfinite(table).all() and (table > 0).all()
+        assert (whole > 0).all()
+        # the partition time is the sum of its layers up to launch gaps
+        ratio = whole / table.sum(axis=0)
+        print("partition / sum(layers):", ratio)
+        assert ((ratio > 0.3) & (ratio < 1.5)).all()
+        recs = part.profile_kernels(8, warmup=3, reps=10)
+        assert len(recs) >= 12 and all(r["mean_us"] > 0 for r in recs)
+        info = part.layer_info(44, 8)
+        assert info["out_bytes_b1"] == 512 * 14 * 14 * 2 and info["flops_b1"] > 0
