@@ -75,6 +75,14 @@ def load_library() -> ctypes.CDLL:
     global _lib
     if _lib is not None:
         return _lib
+    # One HIP runtime per process: PyTorch ships its own libamdhip64.so.7 and
+    # libhsa-runtime64.so.1.  Loading torch first makes the dynamic linker bind
+    # this library to those already-loaded copies (same SONAMEs) instead of a
+    # second runtime from /opt/rocm, which would fight torch over the device.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     if not os.path.exists(LIB_PATH):
         raise PpipeError(-5, f"{LIB_PATH} is not built; run __graft_entry__.build() "
                               "or python paper_2507_18748_amd/build.py")

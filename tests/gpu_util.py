@@ -14,6 +14,8 @@ def _torch():
 
 def upload_nhwc(x_nchw: np.ndarray, dtype: str):
     torch = _torch()
+    if x_nchw.ndim == 2:                       # an FC output: [N, K] is N x K x 1 x 1
+        x_nchw = x_nchw.reshape(x_nchw.shape + (1, 1))
     t = torch.from_numpy(np.ascontiguousarray(x_nchw.transpose(0, 2, 3, 1)))
     return t.to(TORCH_DT[dtype]).cuda().contiguous()
 
