@@ -79,6 +79,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="oracle sample length for cpu_baseline (0 disables)")
     ap.add_argument("--profile-reps", type=int, default=50)
+    ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB mebibytes 10 times "
+                         "(reference for the HBM byte counters) and exit")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -89,6 +92,15 @@ def main():
 
     import numpy as np
     import torch
+    if args.copy_calibration > 0:
+        n = int(args.copy_calibration * 2 ** 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(10):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n * 4, "repeats": 10}))
+        return
     import workloads as W
     from paper_2507_18748_amd import Partition
 
