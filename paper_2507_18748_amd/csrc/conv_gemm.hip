@@ -15,22 +15,32 @@
 //    pixel: the NHWC epilogue stores 8 bytes (16-bit types) per lane.
 //  * 16-bit types use v_mfma_f32_16x16x32_{f16,bf16}; fp32 uses
 //    v_mfma_f32_16x16x4_f32 (full fp32 products, no reduced-precision path).
-//  * Per LDS stage a block stages BM x BK weights and BN x BK activations as
-//    16-byte vectors (rows padded by 16 bytes), double buffered: the next
-//    stage's global loads are issued before the current stage's MFMAs.
+//  * A stage is BM x BK weights plus BN x BK activations (BK = 128 bytes of
+//    K per row), staged through LDS (rows padded by 16 bytes) with two LDS
+//    buffers.  Global loads run DEPTH stages ahead in a ring of register sets
+//    so that DEPTH stages are in flight per block; the small-M layers of a
+//    partition are latency-bound and this is what keeps HBM busy.
 //  * The K order (kh, kw, ci) with ci fastest makes every 16-byte vector of
 //    a row one contiguous NHWC load when C is a multiple of the vector width.
-//    Layers whose C is not (the 3-channel stem) use a scalar gather through
-//    a (kh, kw, ci) lookup table in LDS.
-//  * blockIdx.z splits K; with out_mode 1 each split writes raw fp32 sums
-//    and a separate pass reduces them and applies the epilogue.
+//    Layers whose C is not (the 3-channel stem) gather scalars through a
+//    (kh, kw, ci) lookup table in LDS.
+//  * The 1-D grid is remapped so that the blocks the hardware deals to one
+//    XCD (round-robin over 8) take a contiguous range of tiles: blocks that
+//    read the same weight slice (or the same activation rows) share that
+//    XCD's L2 instead of fetching it once per XCD.
+//  * Layers with few output pixels (small batch, 7x7 / 14x14 maps, fully
+//    connected layers) use a second kernel, see conv_gemm_skinny below.
 #include "kernels.h"
+
+#include <type_traits>
 
 namespace ppipe {
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef _Float16 halfx8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int NUM_XCD = 8;
 
 template <typename T> struct Mfma;
 template <> struct Mfma<_Float16> {
@@ -59,8 +69,6 @@ template <> struct Mfma<float> {
         c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
     }
 };
-
-template <typename T> __device__ __forceinline__ float to_f32(T v) { return (float)v; }
 
 __device__ __forceinline__ float apply_act(float v, int act)
 {
@@ -92,263 +100,25 @@ template <typename T> struct Vec4 {   // 16-bit types
     }
 };
 
-template <typename T, int BM, int BN, int WM, int WN, int KV, bool GENERIC>
-__global__ void __launch_bounds__(WM * WN * 64)
-conv_gemm_kernel(ConvGemmArgs a)
+// c ? v : 0 per component.  A conditional expression on uint4 (a class type)
+// is lowered as a select between two addresses, which forces both operands
+// into scratch memory; scalar selects keep everything in registers.
+__device__ __forceinline__ uint4 keep_if(bool c, const uint4& v)
 {
-    constexpr int NT = WM * WN * 64;
-    constexpr int EPV = 16 / (int)sizeof(T);   // elements per 16-byte vector
-    constexpr int BK = KV * EPV;               // K elements per stage
-    constexpr int ROW = KV * 16 + 16;          // LDS row pitch in bytes
-    constexpr int WTM = BM / WM, WTN = BN / WN;
-    constexpr int FM = WTM / 16, FN = WTN / 16;
-    constexpr int A_VECS = BM * KV, B_VECS = BN * KV;
-    constexpr int A_PER = (A_VECS + NT - 1) / NT;
-    constexpr int B_PER = (B_VECS + NT - 1) / NT;
-    constexpr int B_ELEMS = BN * BK;
-    constexpr int BE_PER = (B_ELEMS + NT - 1) / NT;
-    static_assert(KV % 4 == 0, "a stage holds whole 64-byte MFMA k-steps");
-    static_assert(FM >= 1 && FN >= 1 && WTM % 16 == 0 && WTN % 16 == 0, "wave tile");
-    static_assert(!GENERIC || NT % BK == 0, "generic gather assigns one k column per thread");
+    return make_uint4(c ? v.x : 0u, c ? v.y : 0u, c ? v.z : 0u, c ? v.w : 0u);
+}
 
-    __shared__ __attribute__((aligned(16))) unsigned char smem[2 * (BM + BN) * ROW];
-    __shared__ int ktab[GENERIC ? GEMM_KTAB_MAX : 1];
-
-    const T* __restrict__ X = (const T*)a.x;
-    const T* __restrict__ Wt = (const T*)a.w;
-    const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
-    const int wm = wave % WM, wn = wave / WM;
-    const int m0 = blockIdx.x * BN, co0 = blockIdx.y * BM;
-    const int kc_begin = blockIdx.z * a.chunks_per_split;
-    const int kc_end = min(a.total_chunks, kc_begin + a.chunks_per_split);
-    const int HoWo = a.Ho * a.Wo;
-
-    if constexpr (GENERIC) {
-        for (int k = tid; k < a.Kpad && k < GEMM_KTAB_MAX; k += NT) {
-            int t = -1;
-            if (k < a.K) {
-                int tap = k / a.C, ci = k - tap * a.C;
-                int kh = tap / a.KW, kw = tap - kh * a.KW;
-                t = kh | (kw << 8) | (ci << 16);
-            }
-            ktab[k] = t;
-        }
-        __syncthreads();
-    }
-
-    // ---- per-thread load slots (fixed for the whole K loop) ----
-    int a_row[A_PER], a_kv[A_PER];
-    bool a_ok[A_PER];
-#pragma unroll
-    for (int i = 0; i < A_PER; ++i) {
-        int v = tid + i * NT;
-        a_row[i] = v / KV;
-        a_kv[i] = v % KV;
-        a_ok[i] = v < A_VECS && co0 + a_row[i] < a.Co;
-    }
-    constexpr int BROWS = GENERIC ? BE_PER : B_PER;
-    int b_row[BROWS], b_kv[BROWS], b_hi0[BROWS], b_wi0[BROWS];
-    size_t b_base[BROWS];
-    bool b_ok[BROWS];
-#pragma unroll
-    for (int i = 0; i < BROWS; ++i) {
-        int v = tid + i * NT;
-        int r, kv;
-        bool inrange;
-        if constexpr (GENERIC) {
-            r = v / BK;
-            kv = v % BK;            // here: k column within the stage
-            inrange = v < B_ELEMS;
-        } else {
-            r = v / KV;
-            kv = v % KV;
-            inrange = v < B_VECS;
-        }
-        int m = m0 + r;
-        bool ok = inrange && m < a.M;
-        int mm = ok ? m : 0;
-        int n = mm / HoWo, rem = mm - n * HoWo;
-        int ho = rem / a.Wo, wo = rem - ho * a.Wo;
-        b_row[i] = r;
-        b_kv[i] = kv;
-        b_hi0[i] = ho * a.stride - a.pad;
-        b_wi0[i] = wo * a.stride - a.pad;
-        b_base[i] = (size_t)n * a.H * a.W * a.C;
-        b_ok[i] = ok;
-    }
-
-    uint4 ra[A_PER];
-    uint4 rb[GENERIC ? 1 : B_PER];
-    T rbe[GENERIC ? BE_PER : 1];
-
-    auto load_stage = [&](int kc) {
-        const int k0 = kc * BK;
-#pragma unroll
-        for (int i = 0; i < A_PER; ++i) {
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (a_ok[i])
-                v = *(const uint4*)(Wt + (size_t)(co0 + a_row[i]) * a.Kpad + k0 + a_kv[i] * EPV);
-            ra[i] = v;
-        }
-        if constexpr (GENERIC) {
-#pragma unroll
-            for (int i = 0; i < BE_PER; ++i) {
-                T v = (T)0.0f;
-                int k = k0 + b_kv[i];
-                if (b_ok[i] && k < a.K) {
-                    int t = ktab[k];
-                    int hi = b_hi0[i] + (t & 0xff), wi = b_wi0[i] + ((t >> 8) & 0xff);
-                    if ((unsigned)hi < (unsigned)a.H && (unsigned)wi < (unsigned)a.W)
-                        v = X[b_base[i] + ((size_t)hi * a.W + wi) * a.C + (t >> 16)];
-                }
-                rbe[i] = v;
-            }
-        } else {
-            // the whole stage lies in one (kh, kw) tap: C % BK == 0, or a 1x1 window
-            const int tap = k0 / a.C, ci0 = k0 - tap * a.C;
-            const int kh = tap / a.KW, kw = tap - kh * a.KW;
-#pragma unroll
-            for (int i = 0; i < B_PER; ++i) {
-                uint4 v = make_uint4(0, 0, 0, 0);
-                int ci = ci0 + b_kv[i] * EPV;
-                int hi = b_hi0[i] + kh, wi = b_wi0[i] + kw;
-                if (b_ok[i] && ci < a.C && (unsigned)hi < (unsigned)a.H &&
-                    (unsigned)wi < (unsigned)a.W)
-                    v = *(const uint4*)(X + b_base[i] + ((size_t)hi * a.W + wi) * a.C + ci);
-                rb[i] = v;
-            }
-        }
-    };
-    auto store_stage = [&](int buf) {
-        unsigned char* As = smem + buf * (BM + BN) * ROW;
-        unsigned char* Bs = As + BM * ROW;
-#pragma unroll
-        for (int i = 0; i < A_PER; ++i)
-            if (tid + i * NT < A_VECS)
-                *(uint4*)(As + a_row[i] * ROW + a_kv[i] * 16) = ra[i];
-        if constexpr (GENERIC) {
-#pragma unroll
-            for (int i = 0; i < BE_PER; ++i)
-                if (tid + i * NT < B_ELEMS)
-                    *(T*)(Bs + b_row[i] * ROW + b_kv[i] * (int)sizeof(T)) = rbe[i];
-        } else {
-#pragma unroll
-            for (int i = 0; i < B_PER; ++i)
-                if (tid + i * NT < B_VECS)
-                    *(uint4*)(Bs + b_row[i] * ROW + b_kv[i] * 16) = rb[i];
-        }
-    };
-
-    floatx4 acc[FM][FN];
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-            acc[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
-
-    if (kc_begin < kc_end) {
-        load_stage(kc_begin);
-        store_stage(0);
-        __syncthreads();
-        int buf = 0;
-        for (int kc = kc_begin; kc < kc_end; ++kc) {
-            const bool more = kc + 1 < kc_end;
-            if (more)
-                load_stage(kc + 1);
-            const unsigned char* As = smem + buf * (BM + BN) * ROW;
-            const unsigned char* Bs = As + BM * ROW;
-#pragma unroll
-            for (int ks = 0; ks < KV / 4; ++ks) {
-                uint4 af[FM], bf[FN];
-                const int off = ks * 64 + (lane >> 4) * 16;
-#pragma unroll
-                for (int i = 0; i < FM; ++i)
-                    af[i] = *(const uint4*)(As + (wm * WTM + i * 16 + (lane & 15)) * ROW + off);
-#pragma unroll
-                for (int j = 0; j < FN; ++j)
-                    bf[j] = *(const uint4*)(Bs + (wn * WTN + j * 16 + (lane & 15)) * ROW + off);
-#pragma unroll
-                for (int i = 0; i < FM; ++i)
-#pragma unroll
-                    for (int j = 0; j < FN; ++j)
-                        Mfma<T>::step(af[i], bf[j], acc[i][j]);
-            }
-            if (more)
-                store_stage(buf ^ 1);
-            __syncthreads();
-            buf ^= 1;
-        }
-    }
-
-    // ---- epilogue: lane holds channels co..co+3 of pixel m ----
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-        const int co = co0 + wm * WTM + i * 16 + 4 * (lane >> 4);
-        if (co >= a.Co)
-            continue;
-        float4 sc = make_float4(1.f, 1.f, 1.f, 1.f), bi = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (a.out_mode == 0) {
-            sc = *(const float4*)(a.scale + co);
-            bi = *(const float4*)(a.bias + co);
-        }
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-            const int m = m0 + wn * WTN + j * 16 + (lane & 15);
-            if (m >= a.M)
-                continue;
-            const floatx4 c = acc[i][j];
-            if (a.out_mode == 1) {
-                *(float4*)(a.partial + ((size_t)blockIdx.z * a.M + m) * a.Co + co) =
-                    make_float4(c[0], c[1], c[2], c[3]);
-                continue;
-            }
-            float4 v = make_float4(c[0] * sc.x + bi.x, c[1] * sc.y + bi.y,
-                                   c[2] * sc.z + bi.z, c[3] * sc.w + bi.w);
-            const size_t o = (size_t)m * a.Co + co;
-            if (a.res) {
-                float4 r = Vec4<T>::load((const T*)a.res + o);
-                v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
-            }
-            v.x = apply_act(v.x, a.act); v.y = apply_act(v.y, a.act);
-            v.z = apply_act(v.z, a.act); v.w = apply_act(v.w, a.act);
-            Vec4<T>::store((T*)a.y + o, v);
-        }
+// Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E).  Keeps
+// register-ring indices constant so the ring never lands in scratch memory.
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f)
+{
+    if constexpr (B < E) {
+        f(std::integral_constant<int, B>{});
+        static_for<B + 1, E>(f);
     }
 }
 
-// ---- split-K reduction + epilogue ----
-template <typename T>
-__global__ void __launch_bounds__(256)
-splitk_epilogue_kernel(const float* __restrict__ partial, int splits, int M, int Co,
-                       const float* __restrict__ scale, const float* __restrict__ bias,
-                       const T* __restrict__ res, int act, T* __restrict__ y)
-{
-    const size_t nvec = (size_t)M * Co / 4;
-    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= nvec)
-        return;
-    const float4* p = (const float4*)partial;
-    float4 s = p[i];
-    for (int sp = 1; sp < splits; ++sp) {
-        float4 t = p[(size_t)sp * nvec + i];
-        s.x += t.x; s.y += t.y; s.z += t.z; s.w += t.w;
-    }
-    const int co = (int)((i * 4) % (size_t)Co);
-    const float4 sc = *(const float4*)(scale + co);
-    const float4 bi = *(const float4*)(bias + co);
-    float4 v = make_float4(s.x * sc.x + bi.x, s.y * sc.y + bi.y, s.z * sc.z + bi.z,
-                           s.w * sc.w + bi.w);
-    if (res) {
-        float4 r = Vec4<T>::load(res + i * 4);
-        v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
-    }
-    v.x = apply_act(v.x, act); v.y = apply_act(v.y, act);
-    v.z = apply_act(v.z, act); v.w = apply_act(v.w, act);
-    Vec4<T>::store(y + i * 4, v);
-}
-
-// ---- split-K reduction + bias + softmax, one block per row ----
 __device__ __forceinline__ float wave_max(float v)
 {
 #pragma unroll
@@ -364,125 +134,584 @@ __device__ __forceinline__ float wave_sum(float v)
     return v;
 }
 
-__global__ void __launch_bounds__(256)
-splitk_softmax_kernel(const float* __restrict__ partial, int splits, int M, int O,
-                      const float* __restrict__ bias, float* __restrict__ out)
+// Epilogue of one accumulator fragment row: channels co..co+3 of pixel m.
+template <typename T>
+__device__ __forceinline__ void store_out4(const ConvGemmArgs& a, int co, int m, floatx4 c)
 {
-    __shared__ float z[SOFTMAX_MAX_O];
-    __shared__ float red[4];
-    const int m = blockIdx.x;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const float4 sc = *(const float4*)(a.scale + co);
+    const float4 bi = *(const float4*)(a.bias + co);
+    float4 v = make_float4(c[0] * sc.x + bi.x, c[1] * sc.y + bi.y, c[2] * sc.z + bi.z,
+                           c[3] * sc.w + bi.w);
+    const size_t o = (size_t)m * a.Co + co;
+    if (a.softmax) {
+        *(float4*)(a.logits + o) = v;
+        return;
+    }
+    if (a.res) {
+        float4 r = Vec4<T>::load((const T*)a.res + o);
+        v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
+    }
+    v.x = apply_act(v.x, a.act); v.y = apply_act(v.y, a.act);
+    v.z = apply_act(v.z, a.act); v.w = apply_act(v.w, a.act);
+    Vec4<T>::store((T*)a.y + o, v);
+}
+
+// Tile index -> (m tile, co tile) after spreading the 1-D grid over the XCDs
+// in contiguous ranges (the hardware deals block b to XCD b % 8).
+__device__ __forceinline__ int3 tile_of_block(const ConvGemmArgs& a)
+{
+    const int G = gridDim.x;
+    const int xcd = blockIdx.x % NUM_XCD, slot = blockIdx.x / NUM_XCD;
+    const int per = G / NUM_XCD, rem = G % NUM_XCD;
+    int lin = xcd * per + min(xcd, rem) + slot;
+    const int tiles = a.tiles_m * a.tiles_co;
+    const int split = lin / tiles;
+    lin -= split * tiles;
+    const int fast = a.co_fastest ? a.tiles_co : a.tiles_m;
+    const int q = lin / fast, r = lin - q * fast;
+    return a.co_fastest ? make_int3(q, r, split) : make_int3(r, q, split);   // (m tile, co tile, split)
+}
+
+// ---- buffer loads -------------------------------------------------------
+// Operands are read through buffer resources: a lane whose byte offset is at
+// or beyond the array size gets zeros from the hardware range check.  Zero
+// padding taps, ragged tile rows and the K tail are therefore plain loads at
+// offset OOB, with no branch and no select in the main loop.
+constexpr uint32_t OOB = 0x80000000u;
+constexpr int RSRC_FLAGS = 0x00020000;   // raw buffer, 32-bit data format
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes,
+                                             RSRC_FLAGS);
+}
+__device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t off)
+{
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+template <typename T>
+__device__ __forceinline__ T buf_load_elem(__amdgpu_buffer_rsrc_t r, uint32_t off)
+{
+    if constexpr (sizeof(T) == 4)
+        return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+    else
+        return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0));
+}
+
+// Position of a K step in (kh, kw, ci) order, wave-uniform, advanced by a
+// fixed number of channels; steps never straddle a tap (C is a multiple of the
+// step, or the window is 1x1 and the tail is cut by the channel test).
+struct TapCursor {
+    int ci, kw, kh;
+    __device__ __forceinline__ void start(int k0, int C, int KW)
+    {
+        const int tap = k0 / C;
+        ci = k0 - tap * C;
+        kh = tap / KW;
+        kw = tap - kh * KW;
+    }
+    __device__ __forceinline__ void advance(int step, int C, int KW)
+    {
+        ci += step;
+        if (ci >= C) {
+            ci = 0;
+            if (++kw == KW) {
+                kw = 0;
+                ++kh;
+            }
+        }
+    }
+};
+
+// One output pixel (GEMM column) as seen by the gather: byte offset of its
+// window origin and which kernel rows / columns fall inside the image.
+struct PixelRow {
+    int off;          // bytes of x[n][ho*s - p][wo*s - p][0] (may be negative)
+    uint32_t hmask;   // bit kh set: 0 <= ho*s - p + kh < H
+    uint32_t wmask;   // bit kw set: 0 <= wo*s - p + kw < W
+};
+
+__device__ __forceinline__ PixelRow pixel_row(const ConvGemmArgs& a, int m, int esz)
+{
+    PixelRow p{0, 0u, 0u};
+    if (m >= a.M)
+        return p;
+    const int HoWo = a.Ho * a.Wo;
+    const int n = m / HoWo, rm = m - n * HoWo;
+    const int ho = rm / a.Wo, wo = rm - ho * a.Wo;
+    const int hi0 = ho * a.stride - a.pad, wi0 = wo * a.stride - a.pad;
+    p.off = (((n * a.H + hi0) * a.W + wi0) * a.C) * esz;
+    for (int kh = 0; kh < a.KH; ++kh)
+        if ((unsigned)(hi0 + kh) < (unsigned)a.H) p.hmask |= 1u << kh;
+    for (int kw = 0; kw < a.KW; ++kw)
+        if ((unsigned)(wi0 + kw) < (unsigned)a.W) p.wmask |= 1u << kw;
+    return p;
+}
+
+// LDS-staged implicit GEMM for layers with many output pixels.
+template <typename T, int BM, int BN, int WM, int WN, int KV, int DEPTH, bool GENERIC>
+__global__ void __launch_bounds__(WM * WN * 64)
+conv_gemm_kernel(ConvGemmArgs a)
+{
+    constexpr int NT = WM * WN * 64;
+    constexpr int ESZ = (int)sizeof(T);
+    constexpr int EPV = 16 / ESZ;              // elements per 16-byte vector
+    constexpr int BK = KV * EPV;               // K elements per stage
+    constexpr int ROW = KV * 16 + 16;          // LDS row pitch in bytes
+    constexpr int WTM = BM / WM, WTN = BN / WN;
+    constexpr int FM = WTM / 16, FN = WTN / 16;
+    constexpr int A_VECS = BM * KV, B_VECS = BN * KV;
+    constexpr int A_PER = (A_VECS + NT - 1) / NT;
+    constexpr int B_PER = (B_VECS + NT - 1) / NT;
+    constexpr int B_ELEMS = BN * BK;
+    constexpr int BE_PER = (B_ELEMS + NT - 1) / NT;
+    constexpr int STAGE = (BM + BN) * ROW;
+    constexpr int RB = GENERIC ? 1 : B_PER, RBE = GENERIC ? BE_PER : 1;
+    static_assert(KV % 4 == 0, "a stage holds whole 64-byte MFMA k-steps");
+    static_assert(FM >= 1 && FN >= 1 && WTM % 16 == 0 && WTN % 16 == 0, "wave tile");
+    static_assert(DEPTH == 2, "the LDS pipeline keeps two register sets in flight");
+
+    __shared__ __attribute__((aligned(16))) unsigned char smem[2 * STAGE];
+    __shared__ int ktab[GENERIC ? GEMM_KTAB_MAX : 1];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int wm = wave % WM, wn = wave / WM;
+    const int3 tt = tile_of_block(a);
+    const int m0 = tt.x * BN, co0 = tt.y * BM;
+    const int kc_begin = tt.z * a.chunks_per_split;
+    const int kc_end = min(a.total_chunks, kc_begin + a.chunks_per_split);
+    const int nst = kc_end - kc_begin;
+    const auto wsrc = make_rsrc(a.w, (uint32_t)a.Co * a.Kpad * ESZ);
+    const auto xsrc = make_rsrc(a.x, (uint32_t)a.N * a.H * a.W * a.C * ESZ);
+
+    if constexpr (GENERIC) {
+        for (int k = tid; k < a.Kpad && k < GEMM_KTAB_MAX; k += NT) {
+            int t = -1;
+            if (k < a.K) {
+                int tap = k / a.C, ci = k - tap * a.C;
+                int kh = tap / a.KW, kw = tap - kh * a.KW;
+                t = kh | (kw << 8) | (ci << 16);
+            }
+            ktab[k] = t;
+        }
+        __syncthreads();
+    }
+
+    // ---- per-thread load slots, fixed for the whole K loop ----
+    uint32_t a_off[A_PER];
+    int a_lds[A_PER];
+#pragma unroll
+    for (int i = 0; i < A_PER; ++i) {
+        const int v = tid + i * NT, row = v / KV, kv = v % KV;
+        const bool ok = v < A_VECS && co0 + row < a.Co;
+        a_off[i] = ok ? (uint32_t)(((co0 + row) * a.Kpad + kv * EPV) * ESZ) : OOB;
+        a_lds[i] = row * ROW + kv * 16;
+    }
+    constexpr int BROWS = GENERIC ? BE_PER : B_PER;
+    PixelRow b_px[BROWS];
+    int b_k[BROWS], b_lds[BROWS];
+#pragma unroll
+    for (int i = 0; i < BROWS; ++i) {
+        const int v = tid + i * NT;
+        const int r = GENERIC ? v / BK : v / KV;
+        const int kk = GENERIC ? v % BK : v % KV;   // k column (gather) or 16-byte vector
+        const bool inrange = v < (GENERIC ? B_ELEMS : B_VECS);
+        b_px[i] = pixel_row(a, inrange ? m0 + r : a.M, ESZ);
+        b_k[i] = kk;
+        b_lds[i] = BM * ROW + r * ROW + (GENERIC ? kk * ESZ : kk * 16);
+    }
+
+    // register ring: two sets, DEPTH stages in flight
+    uint4 ra0[A_PER], ra1[A_PER], rb0[RB], rb1[RB];
+    T re0[RBE], re1[RBE];
+    TapCursor cur;              // (kh, kw, ci) of the next stage to load
+    int lst = kc_begin;         // its stage index
+    cur.start(kc_begin * BK, a.C, a.KW);
+
+    auto load_stage = [&](uint4 (&sa)[A_PER], uint4 (&sb)[RB], T (&se)[RBE]) {
+        const uint32_t k0b = (uint32_t)(lst * BK * ESZ);
+#pragma unroll
+        for (int i = 0; i < A_PER; ++i)
+            sa[i] = buf_load16(wsrc, a_off[i] + k0b);
+        if constexpr (GENERIC) {
+            const int k0 = lst * BK;
+#pragma unroll
+            for (int i = 0; i < BE_PER; ++i) {
+                const int k = k0 + b_k[i];
+                const int t = k < a.K ? ktab[k] : 0;
+                const int kh = t & 0xff, kw = (t >> 8) & 0xff, ci = t >> 16;
+                const bool ok = k < a.K && ((b_px[i].hmask >> kh) & (b_px[i].wmask >> kw) & 1u);
+                se[i] = buf_load_elem<T>(
+                    xsrc, ok ? (uint32_t)(b_px[i].off + ((kh * a.W + kw) * a.C + ci) * ESZ) : OOB);
+            }
+        } else {
+            const int tap_off = ((cur.kh * a.W + cur.kw) * a.C + cur.ci) * ESZ;
+            const int cleft = a.C - cur.ci;
+#pragma unroll
+            for (int i = 0; i < B_PER; ++i) {
+                const bool ok = ((b_px[i].hmask >> cur.kh) & (b_px[i].wmask >> cur.kw) & 1u) &&
+                                b_k[i] * EPV < cleft;
+                sb[i] = buf_load16(xsrc, ok ? (uint32_t)(b_px[i].off + tap_off + b_k[i] * 16) : OOB);
+            }
+        }
+        if (lst < kc_end - 1) { // past the last stage the same stage is reloaded
+            ++lst;
+            cur.advance(BK, a.C, a.KW);
+        }
+    };
+    auto store_stage = [&](unsigned char* S, const uint4 (&sa)[A_PER], const uint4 (&sb)[RB],
+                           const T (&se)[RBE]) {
+#pragma unroll
+        for (int i = 0; i < A_PER; ++i)
+            if (tid + i * NT < A_VECS)
+                *(uint4*)(S + a_lds[i]) = sa[i];
+        if constexpr (GENERIC) {
+#pragma unroll
+            for (int i = 0; i < BE_PER; ++i)
+                if (tid + i * NT < B_ELEMS)
+                    *(T*)(S + b_lds[i]) = se[i];
+        } else {
+#pragma unroll
+            for (int i = 0; i < B_PER; ++i)
+                if (tid + i * NT < B_VECS)
+                    *(uint4*)(S + b_lds[i]) = sb[i];
+        }
+    };
+
+    floatx4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+            acc[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    // fragment read offsets within a stage
+    int fa[FM], fb[FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) fa[i] = (wm * WTM + i * 16 + (lane & 15)) * ROW + (lane >> 4) * 16;
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+        fb[j] = BM * ROW + (wn * WTN + j * 16 + (lane & 15)) * ROW + (lane >> 4) * 16;
+
+    // One pipeline step on stage s: refill the register set that held stage s
+    // (it went to LDS last step) with stage s + 2, run the MFMAs on LDS buffer
+    // s & 1, then move the other set (stage s + 1) into the other LDS buffer.
+    // A macro over two named sets keeps every register index a constant.
+#define PPIPE_STEP(s, A0, B0, E0, A1, B1, E1)                                                    \
+    do {                                                                                          \
+        load_stage(A0, B0, E0);                                                                   \
+        const unsigned char* S = smem + ((s) & 1) * STAGE;                                        \
+        _Pragma("unroll") for (int ks = 0; ks < KV / 4; ++ks) {                                   \
+            uint4 af[FM], bf[FN];                                                                 \
+            _Pragma("unroll") for (int i = 0; i < FM; ++i)                                        \
+                af[i] = *(const uint4*)(S + fa[i] + ks * 64);                                     \
+            _Pragma("unroll") for (int j = 0; j < FN; ++j)                                        \
+                bf[j] = *(const uint4*)(S + fb[j] + ks * 64);                                     \
+            _Pragma("unroll") for (int i = 0; i < FM; ++i)                                        \
+                _Pragma("unroll") for (int j = 0; j < FN; ++j)                                    \
+                    Mfma<T>::step(af[i], bf[j], acc[i][j]);                                       \
+        }                                                                                         \
+        if ((s) + 1 < nst)                                                                        \
+            store_stage(smem + (((s) + 1) & 1) * STAGE, A1, B1, E1);                              \
+        __syncthreads();                                                                          \
+    } while (0)
+    if (nst > 0) {
+        load_stage(ra0, rb0, re0);
+        load_stage(ra1, rb1, re1);
+        store_stage(smem, ra0, rb0, re0);
+        __syncthreads();
+        for (int s0 = 0; s0 < nst; s0 += 2) {
+            PPIPE_STEP(s0, ra0, rb0, re0, ra1, rb1, re1);
+            if (s0 + 1 < nst)
+                PPIPE_STEP(s0 + 1, ra1, rb1, re1, ra0, rb0, re0);
+        }
+    }
+#undef PPIPE_STEP
+
+    // ---- epilogue: lane holds channels co..co+3 of pixel m ----
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int co = co0 + wm * WTM + i * 16 + 4 * (lane >> 4);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int m = m0 + wn * WTN + j * 16 + (lane & 15);
+            if (co >= a.Co || m >= a.M)
+                continue;
+            if (a.splits > 1) {   // raw sums; splitk_reduce applies the epilogue
+                const floatx4 c = acc[i][j];
+                *(float4*)(a.partial + ((size_t)tt.z * a.M + m) * a.Co + co) =
+                    make_float4(c[0], c[1], c[2], c[3]);
+            } else {
+                store_out4<T>(a, co, m, acc[i][j]);
+            }
+        }
+    }
+}
+
+// Split-K reduction: one thread per 4 output channels of one pixel, partials
+// summed in split order (bitwise deterministic), then the layer epilogue.
+template <typename T>
+__global__ void __launch_bounds__(256) splitk_reduce_kernel(ConvGemmArgs a)
+{
+    const size_t nvec = (size_t)a.M * a.Co / 4;
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= nvec)
+        return;
+    const float4* p = (const float4*)a.partial;
+    float4 t = p[i];
+    for (int sp = 1; sp < a.splits; ++sp) {
+        const float4 v = p[(size_t)sp * nvec + i];
+        t.x += v.x; t.y += v.y; t.z += v.z; t.w += v.w;
+    }
+    const int co = (int)((i * 4) % (size_t)a.Co);
+    const int m = (int)((i * 4) / (size_t)a.Co);
+    store_out4<T>(a, co, m, floatx4{t.x, t.y, t.z, t.w});
+}
+
+// Skinny implicit GEMM for layers with few output pixels.
+//
+// A block of WK waves owns one (16*FM) x (16*FN) output tile; wave w reduces
+// a contiguous slice of the K steps (a K step is 64 bytes of every operand
+// row: one 16x16x32 MFMA for 16-bit types, four 16x16x4 for fp32).  Each MFMA
+// operand fragment is one 16-byte buffer load per lane straight from global
+// memory: row (lane % 16) of the weights or of the gathered activations, at
+// k offset 16 * (lane / 16) bytes, so there is no LDS staging and no block
+// barrier in the K loop.  Loads run DEPTH steps ahead in a register ring.
+// The WK partial tiles are summed through LDS in wave order, deterministically.
+template <typename T, int FM, int FN, int WK, int DEPTH>
+__global__ void __launch_bounds__(WK * 64)
+conv_gemm_skinny(ConvGemmArgs a)
+{
+    constexpr int ESZ = (int)sizeof(T);
+    constexpr int EPV = 16 / ESZ;
+    constexpr int KS = 4 * EPV;               // K elements per step
+    constexpr int NF = FM + FN;
+    __shared__ floatx4 red[WK][FM * FN][64];
+
+    const int lane = threadIdx.x & 63;
+    // wave-uniform: keeps the K-step and tap arithmetic on the scalar unit
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int g = lane >> 4, r = lane & 15;
+    const int3 tt = tile_of_block(a);
+    const int m0 = tt.x * 16 * FN, co0 = tt.y * 16 * FM;
+    const auto wsrc = make_rsrc(a.w, (uint32_t)a.Co * a.Kpad * ESZ);
+    const auto xsrc = make_rsrc(a.x, (uint32_t)a.N * a.H * a.W * a.C * ESZ);
+
+    // this wave's K steps [u0, u1)
+    const int U = a.total_chunks;
+    const int u0 = (int)((long)U * wave / WK), u1 = (int)((long)U * (wave + 1) / WK);
+
+    uint32_t a_off[FM];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int co = co0 + i * 16 + r;
+        a_off[i] = co < a.Co ? (uint32_t)((co * a.Kpad + g * EPV) * ESZ) : OOB;
+    }
+    PixelRow px[FN];
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+        px[j] = pixel_row(a, m0 + j * 16 + r, ESZ);
+        px[j].off += g * 16;
+    }
+    const int gk = g * EPV;     // this lane's first channel within a step
+
+    TapCursor cur;
+    int lu = u0;
+    cur.start(u0 * KS, a.C, a.KW);
+    auto load = [&](uint4 (&v)[NF]) {
+        const uint32_t k0b = (uint32_t)(lu * KS * ESZ);
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+            v[i] = buf_load16(wsrc, a_off[i] + k0b);
+        const int tap_off = ((cur.kh * a.W + cur.kw) * a.C + cur.ci) * ESZ;
+        const bool chan_ok = gk < a.C - cur.ci;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const bool ok = chan_ok && ((px[j].hmask >> cur.kh) & (px[j].wmask >> cur.kw) & 1u);
+            v[FM + j] = buf_load16(xsrc, ok ? (uint32_t)(px[j].off + tap_off) : OOB);
+        }
+        if (lu < u1 - 1) {
+            ++lu;
+            cur.advance(KS, a.C, a.KW);
+        }
+    };
+
+    floatx4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+            acc[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+    auto compute = [&](const uint4 (&v)[NF]) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+                Mfma<T>::step(v[i], v[FM + j], acc[i][j]);
+    };
+
+    uint4 ring[DEPTH][NF];
+    if (u0 < u1) {
+        static_for<0, DEPTH>([&](auto dc) { load(ring[decltype(dc)::value]); });
+        int u = u0;
+        for (; u + DEPTH <= u1; u += DEPTH) {
+            static_for<0, DEPTH>([&](auto dc) {
+                constexpr int d = decltype(dc)::value;
+                compute(ring[d]);
+                load(ring[d]);
+            });
+        }
+        static_for<0, DEPTH>([&](auto dc) {
+            constexpr int d = decltype(dc)::value;
+            if (u + d < u1)
+                compute(ring[d]);
+        });
+    }
+
+    // ---- reduce the WK partial tiles in wave order, then the epilogue ----
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+            red[wave][i * FN + j][lane] = acc[i][j];
+    __syncthreads();
+    for (int f = wave; f < FM * FN; f += WK) {
+        floatx4 t = red[0][f][lane];
+        for (int w = 1; w < WK; ++w)
+            t += red[w][f][lane];
+        const int i = f / FN, j = f - (f / FN) * FN;
+        const int co = co0 + i * 16 + 4 * g;
+        const int m = m0 + j * 16 + r;
+        if (co < a.Co && m < a.M)
+            store_out4<T>(a, co, m, t);
+    }
+}
+
+// Softmax of each row of fp32 logits; one wave per row.
+__global__ void __launch_bounds__(256)
+softmax_rows_kernel(const float* __restrict__ z, int M, int O, float* __restrict__ out)
+{
+    const int lane = threadIdx.x & 63;
+    const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (m >= M)
+        return;
+    const float* zr = z + (size_t)m * O;
     float mx = -INFINITY;
-    for (int o = tid; o < O; o += 256) {
-        float s = bias ? bias[o] : 0.0f;
-        for (int sp = 0; sp < splits; ++sp)
-            s += partial[((size_t)sp * M + m) * O + o];
-        z[o] = s;
-        mx = fmaxf(mx, s);
-    }
+    for (int o = lane; o < O; o += 64)
+        mx = fmaxf(mx, zr[o]);
     mx = wave_max(mx);
-    if (lane == 0)
-        red[wave] = mx;
-    __syncthreads();
-    mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
-    __syncthreads();
     float sum = 0.0f;
-    for (int o = tid; o < O; o += 256) {
-        float e = expf(z[o] - mx);
-        z[o] = e;
-        sum += e;
-    }
-    sum = wave_sum(sum);
-    if (lane == 0)
-        red[wave] = sum;
-    __syncthreads();
-    const float inv = 1.0f / (red[0] + red[1] + red[2] + red[3]);
-    for (int o = tid; o < O; o += 256)
-        out[(size_t)m * O + o] = z[o] * inv;
+    for (int o = lane; o < O; o += 64)
+        sum += expf(zr[o] - mx);
+    const float inv = 1.0f / wave_sum(sum);
+    for (int o = lane; o < O; o += 64)
+        out[(size_t)m * O + o] = expf(zr[o] - mx) * inv;
 }
 
 // ---- host-side launchers ----
 GemmCfgInfo gemm_cfg_info(int cfg)
 {
     switch (cfg) {
-    case GEMM_128x128: return {128, 128, 256, 4};
-    case GEMM_64x64:   return {64, 64, 256, 4};
-    case GEMM_64x16:   return {64, 16, 256, 4};
-    default:           return {0, 0, 0, 0};
+    case GEMM_128x128:  return {128, 128, 8, false};
+    case GEMM_64x64:    return {64, 64, 8, false};
+    case GEMM_64x128:   return {64, 128, 8, false};
+    case GEMM_SK_32x32: return {32, 32, 4, true};
+    case GEMM_SK_32x16: return {32, 16, 4, true};
+    case GEMM_SK_16x32: return {16, 32, 4, true};
+    case GEMM_SK_16x16: return {16, 16, 4, true};
+    default:            return {0, 0, 0, false};
     }
 }
 
-template <typename T, int BM, int BN, int WM, int WN, int KV>
-static hipError_t launch_t(bool generic, const ConvGemmArgs& a, int splits, hipStream_t s)
+template <typename T, int BM, int BN, int WM, int WN, int KV, int DEPTH>
+static hipError_t launch_lds(bool generic, const ConvGemmArgs& a, hipStream_t s)
 {
-    dim3 grid((a.M + BN - 1) / BN, (a.Co + BM - 1) / BM, splits);
+    dim3 grid((unsigned)(a.tiles_m * a.tiles_co * a.splits));
     dim3 block(WM * WN * 64);
     if (generic)
-        hipLaunchKernelGGL((conv_gemm_kernel<T, BM, BN, WM, WN, KV, true>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((conv_gemm_kernel<T, BM, BN, WM, WN, KV, DEPTH, true>), grid, block,
+                           0, s, a);
     else
-        hipLaunchKernelGGL((conv_gemm_kernel<T, BM, BN, WM, WN, KV, false>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((conv_gemm_kernel<T, BM, BN, WM, WN, KV, DEPTH, false>), grid, block,
+                           0, s, a);
+    return hipGetLastError();
+}
+
+template <typename T, int FM, int FN>
+static hipError_t launch_skinny(int wk, const ConvGemmArgs& a, hipStream_t s)
+{
+    dim3 grid((unsigned)(a.tiles_m * a.tiles_co));
+    switch (wk) {
+    case 4:
+        hipLaunchKernelGGL((conv_gemm_skinny<T, FM, FN, 4, 8>), grid, dim3(256), 0, s, a);
+        break;
+    case 8:
+        hipLaunchKernelGGL((conv_gemm_skinny<T, FM, FN, 8, 8>), grid, dim3(512), 0, s, a);
+        break;
+    case 16:   // 1024 threads: only the 16x16 tile fits the register file
+        if constexpr (FM * FN == 1) {
+            hipLaunchKernelGGL((conv_gemm_skinny<T, FM, FN, 16, 8>), grid, dim3(1024), 0, s, a);
+            break;
+        }
+        return hipErrorInvalidValue;
+    default:
+        return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 
 template <typename T>
-static hipError_t launch_cfg(int cfg, bool generic, const ConvGemmArgs& a, int splits,
+static hipError_t launch_cfg(int cfg, int wk, bool generic, const ConvGemmArgs& a,
                              hipStream_t s)
 {
+    if (gemm_cfg_info(cfg).skinny && generic)
+        return hipErrorInvalidValue;
     switch (cfg) {
-    case GEMM_128x128: return launch_t<T, 128, 128, 2, 2, 4>(generic, a, splits, s);
-    case GEMM_64x64:   return launch_t<T, 64, 64, 2, 2, 4>(generic, a, splits, s);
-    case GEMM_64x16:   return launch_t<T, 64, 16, 4, 1, 4>(generic, a, splits, s);
-    default:           return hipErrorInvalidValue;
+    case GEMM_128x128:  return launch_lds<T, 128, 128, 2, 2, 8, 2>(generic, a, s);
+    case GEMM_64x64:    return launch_lds<T, 64, 64, 2, 2, 8, 2>(generic, a, s);
+    case GEMM_64x128:   return launch_lds<T, 64, 128, 2, 2, 8, 2>(generic, a, s);
+    case GEMM_SK_32x32: return launch_skinny<T, 2, 2>(wk, a, s);
+    case GEMM_SK_32x16: return launch_skinny<T, 2, 1>(wk, a, s);
+    case GEMM_SK_16x32: return launch_skinny<T, 1, 2>(wk, a, s);
+    case GEMM_SK_16x16: return launch_skinny<T, 1, 1>(wk, a, s);
+    default:            return hipErrorInvalidValue;
     }
 }
 
-hipError_t launch_conv_gemm(int dt, int cfg, bool generic, const ConvGemmArgs& a,
-                            int splits, hipStream_t s)
+hipError_t launch_conv_gemm(int dt, int cfg, int wk, bool generic, const ConvGemmArgs& a,
+                            hipStream_t s)
 {
     switch (dt) {
-    case DT_F32:  return launch_cfg<float>(cfg, generic, a, splits, s);
-    case DT_F16:  return launch_cfg<_Float16>(cfg, generic, a, splits, s);
-    case DT_BF16: return launch_cfg<__bf16>(cfg, generic, a, splits, s);
+    case DT_F32:  return launch_cfg<float>(cfg, wk, generic, a, s);
+    case DT_F16:  return launch_cfg<_Float16>(cfg, wk, generic, a, s);
+    case DT_BF16: return launch_cfg<__bf16>(cfg, wk, generic, a, s);
     default:      return hipErrorInvalidValue;
     }
 }
 
-static const char* dt_name(int dt)
+hipError_t launch_softmax_rows(const float* logits, int M, int O, float* out, hipStream_t s)
 {
-    return dt == DT_F32 ? "f32" : dt == DT_F16 ? "f16" : "bf16";
+    hipLaunchKernelGGL(softmax_rows_kernel, dim3((M + 3) / 4), dim3(256), 0, s, logits, M, O,
+                       out);
+    return hipGetLastError();
 }
 
-const char* conv_gemm_name(int dt, int cfg, bool generic)
-{
-    static char names[3][GEMM_NCFG][2][64];
-    char* n = names[dt][cfg][generic ? 1 : 0];
-    if (!n[0]) {
-        GemmCfgInfo c = gemm_cfg_info(cfg);
-        snprintf(n, 64, "conv_gemm<%s,%dx%d,kv%d%s>", dt_name(dt), c.bm, c.bn, c.kv,
-                 generic ? ",gather" : "");
-    }
-    return n;
-}
+const char* softmax_rows_name() { return "softmax_rows<f32>"; }
 
-hipError_t launch_splitk_epilogue(int dt, const float* partial, int splits, int M, int Co,
-                                  const float* scale, const float* bias, const void* res,
-                                  int act, void* y, hipStream_t s)
+hipError_t launch_splitk_reduce(int dt, const ConvGemmArgs& a, hipStream_t s)
 {
-    const size_t nvec = (size_t)M * Co / 4;
-    dim3 grid((unsigned)((nvec + 255) / 256)), block(256);
+    const size_t nvec = (size_t)a.M * a.Co / 4;
+    const dim3 grid((unsigned)((nvec + 255) / 256)), block(256);
     switch (dt) {
     case DT_F32:
-        hipLaunchKernelGGL(splitk_epilogue_kernel<float>, grid, block, 0, s, partial, splits,
-                           M, Co, scale, bias, (const float*)res, act, (float*)y);
+        hipLaunchKernelGGL(splitk_reduce_kernel<float>, grid, block, 0, s, a);
         break;
     case DT_F16:
-        hipLaunchKernelGGL(splitk_epilogue_kernel<_Float16>, grid, block, 0, s, partial,
-                           splits, M, Co, scale, bias, (const _Float16*)res, act,
-                           (_Float16*)y);
+        hipLaunchKernelGGL(splitk_reduce_kernel<_Float16>, grid, block, 0, s, a);
         break;
     case DT_BF16:
-        hipLaunchKernelGGL(splitk_epilogue_kernel<__bf16>, grid, block, 0, s, partial,
-                           splits, M, Co, scale, bias, (const __bf16*)res, act, (__bf16*)y);
+        hipLaunchKernelGGL(splitk_reduce_kernel<__bf16>, grid, block, 0, s, a);
         break;
     default:
         return hipErrorInvalidValue;
@@ -490,21 +719,31 @@ hipError_t launch_splitk_epilogue(int dt, const float* partial, int splits, int 
     return hipGetLastError();
 }
 
-const char* splitk_epilogue_name(int dt)
+const char* splitk_reduce_name(int dt)
 {
-    static const char* n[3] = {"splitk_epilogue<f32>", "splitk_epilogue<f16>",
-                               "splitk_epilogue<bf16>"};
+    static const char* n[3] = {"splitk_reduce<f32>", "splitk_reduce<f16>", "splitk_reduce<bf16>"};
     return n[dt];
 }
 
-hipError_t launch_splitk_softmax(const float* partial, int splits, int M, int O,
-                                 const float* bias, float* out, hipStream_t s)
+static const char* dt_name(int dt)
 {
-    hipLaunchKernelGGL(splitk_softmax_kernel, dim3(M), dim3(256), 0, s, partial, splits, M,
-                       O, bias, out);
-    return hipGetLastError();
+    return dt == DT_F32 ? "f32" : dt == DT_F16 ? "f16" : "bf16";
 }
 
-const char* splitk_softmax_name() { return "splitk_softmax<f32>"; }
+const char* conv_gemm_name(int dt, int cfg, int wk, bool generic)
+{
+    static char names[3][GEMM_NCFG][SKINNY_MAX_WAVES + 1][2][64];
+    const GemmCfgInfo c = gemm_cfg_info(cfg);
+    const int w = c.skinny ? wk : 0;
+    char* n = names[dt][cfg][w][generic ? 1 : 0];
+    if (!n[0]) {
+        if (c.skinny)
+            snprintf(n, 64, "conv_gemm_skinny<%s,%dx%d,waves%d>", dt_name(dt), c.bm, c.bn, wk);
+        else
+            snprintf(n, 64, "conv_gemm<%s,%dx%d,kv%d%s>", dt_name(dt), c.bm, c.bn, c.kv,
+                     generic ? ",gather" : "");
+    }
+    return n;
+}
 
 }  // namespace ppipe

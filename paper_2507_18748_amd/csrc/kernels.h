@@ -18,56 +18,74 @@ inline int dtype_size(int dt) { return dt == DT_F32 ? 4 : 2; }
 //   reduction    k = (kh, kw, ci) in [0, K), K = KH * KW * C
 // Weights are packed [Co][Kpad] in the storage dtype with k ordered (kh, kw, ci)
 // and zero padding up to Kpad (a multiple of 64 elements).
+// Softmax mode writes fp32 logits (scale * sum + bias) to `logits` instead of
+// the activation epilogue; launch_softmax_rows then normalises them.
 struct ConvGemmArgs {
     const void* x;        // [N][H][W][C]
     const void* w;        // [Co][Kpad]
     const float* scale;   // [Co] folded batch-norm scale (1 without BN)
     const float* bias;    // [Co] folded shift
     const void* res;      // [M][Co] residual in dtype, or nullptr
-    void* y;              // [M][Co] output in dtype (out_mode 0)
-    float* partial;       // [splits][M][Co] fp32 (out_mode 1)
+    void* y;              // [M][Co] output in dtype
+    float* logits;        // [M][Co] fp32 (softmax mode)
+    float* partial;       // [splits][M][Co] fp32 raw sums (LDS kernel with splits > 1)
     int N, H, W, C;
     int Ho, Wo, Co;
     int KH, KW, stride, pad;
     int K, Kpad, M;
     int act;
-    int total_chunks;     // ceil(K / BK)
-    int chunks_per_split; // BK chunks handled by each blockIdx.z
-    int out_mode;         // 0: fused epilogue into y; 1: raw fp32 sums into partial[split]
+    int total_chunks;     // LDS kernel: ceil(K / BK); skinny kernel: ceil(K / KS)
+    int splits;           // LDS kernel: K ranges per tile (blockIdx spans tiles x splits)
+    int chunks_per_split;
+    int tiles_m, tiles_co;
+    int co_fastest;       // tile order: 0 = m tiles of one weight slice adjacent, 1 = co tiles adjacent
+    int softmax;          // 1: write fp32 logits for a following softmax
 };
 
-// Tile configurations of the MFMA kernel (rows = co, columns = m).
+// Tile configurations (rows = co, columns = m).
+//   LDS-tiled kernel for large M: blocks of 4 waves share staged tiles.
+//   Skinny kernel for small M: a block of WK waves computes one small tile,
+//   each wave a slice of K, operands loaded straight into registers.
 enum GemmCfg : int {
-    GEMM_128x128 = 0,   // 4 waves, 64x64 per wave
-    GEMM_64x64 = 1,     // 4 waves, 32x32 per wave
-    GEMM_64x16 = 2,     // 4 waves, 16x16 per wave (small M: FC at batch <= 16)
-    GEMM_NCFG = 3
+    GEMM_128x128 = 0,   // LDS, 4 waves, 64x64 per wave
+    GEMM_64x64 = 1,     // LDS, 4 waves, 32x32 per wave
+    GEMM_64x128 = 2,    // LDS, 4 waves, 32x64 per wave (64 output channels, many pixels)
+    GEMM_SK_32x32 = 3,  // skinny 32x32 tile
+    GEMM_SK_32x16 = 4,  // skinny 32 co x 16 m
+    GEMM_SK_16x32 = 5,  // skinny 16 co x 32 m
+    GEMM_SK_16x16 = 6,  // skinny 16x16 tile
+    GEMM_NCFG = 7
 };
 struct GemmCfgInfo {
-    int bm, bn, threads, kv;   // kv: 16-byte vectors of K per LDS stage
+    int bm, bn, kv;       // tile rows (co), columns (m); kv: 16-byte vectors of K per LDS stage
+    bool skinny;
 };
 GemmCfgInfo gemm_cfg_info(int cfg);
-inline int gemm_bk(int cfg, int dt) { return gemm_cfg_info(cfg).kv * (16 / dtype_size(dt)); }
+// K elements per pipeline step: an LDS stage, or one 64-byte MFMA k-step (skinny)
+inline int gemm_bk(int cfg, int dt)
+{
+    const GemmCfgInfo c = gemm_cfg_info(cfg);
+    return (c.skinny ? 4 : c.kv) * (16 / dtype_size(dt));
+}
 
 // Largest K (elements) the generic (scalar-gather) path supports.
 constexpr int GEMM_KTAB_MAX = 2048;
-
-hipError_t launch_conv_gemm(int dt, int cfg, bool generic, const ConvGemmArgs& a,
-                            int splits, hipStream_t s);
-const char* conv_gemm_name(int dt, int cfg, bool generic);
-
-// Sum of split-K partials followed by the conv epilogue (scale, bias,
-// residual, activation, rounding to dtype).  Co % 4 == 0.
-hipError_t launch_splitk_epilogue(int dt, const float* partial, int splits, int M, int Co,
-                                  const float* scale, const float* bias, const void* res,
-                                  int act, void* y, hipStream_t s);
-const char* splitk_epilogue_name(int dt);
-
-// Sum of split-K partials + bias, then softmax over each row; fp32 output [M][O].
 constexpr int SOFTMAX_MAX_O = 8192;
-hipError_t launch_splitk_softmax(const float* partial, int splits, int M, int O,
-                                 const float* bias, float* out, hipStream_t s);
-const char* splitk_softmax_name();
+constexpr int SKINNY_MAX_WAVES = 16;
+
+// wk: waves per block of the skinny kernel (K split), ignored by the LDS kernel.
+hipError_t launch_conv_gemm(int dt, int cfg, int wk, bool generic, const ConvGemmArgs& a,
+                            hipStream_t s);
+const char* conv_gemm_name(int dt, int cfg, int wk, bool generic);
+
+// Sum of the split-K partials in split order, then the layer epilogue
+// (scale, bias, residual, activation, rounding; or fp32 logits in softmax mode).
+hipError_t launch_splitk_reduce(int dt, const ConvGemmArgs& a, hipStream_t s);
+const char* splitk_reduce_name(int dt);
+
+// Row-wise softmax of fp32 logits [M][O] into out [M][O].
+hipError_t launch_softmax_rows(const float* logits, int M, int O, float* out, hipStream_t s);
+const char* softmax_rows_name();
 
 // Depthwise k x k convolution (NHWC, weights [k][k][C] in dtype) with the
 // folded batch norm and activation.  C % (16 / sizeof(dtype)) == 0.

@@ -135,30 +135,46 @@ maxpool_kernel(const T* __restrict__ x, T* __restrict__ y, int N, int H, int W, 
     Vec16<T>::store(y + (((size_t)n * Ho + ho) * Wo + wo) * C + c, m);
 }
 
+// Global average pool: a block owns 32 channel vectors (256 or 128 channels)
+// of one image; its 8 thread rows split the H*W pixels, so every pixel row of
+// the block is one contiguous 512-byte read, and the 8 partial sums are added
+// through LDS in a fixed order.
 template <typename T>
 __global__ void __launch_bounds__(256)
 gap_kernel(const T* __restrict__ x, T* __restrict__ y, int N, int HW, int C)
 {
     constexpr int V = Vec16<T>::N;
+    __shared__ float part[8][32][V + 1];
     const int CV = C / V;
-    const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= (size_t)N * CV)
-        return;
-    const int cv = (int)(idx % CV), n = (int)(idx / CV);
+    const int cv = blockIdx.x % ((CV + 31) / 32) * 32 + (threadIdx.x & 31);
+    const int n = blockIdx.x / ((CV + 31) / 32);
+    const int pr = threadIdx.x >> 5;    // pixel row 0..7
     float s[V];
 #pragma unroll
     for (int i = 0; i < V; ++i) s[i] = 0.0f;
-    const T* p = x + (size_t)n * HW * C + cv * V;
-    for (int t = 0; t < HW; ++t) {
-        float v[V];
-        Vec16<T>::load(p + (size_t)t * C, v);
+    if (cv < CV) {
+        const T* p = x + (size_t)n * HW * C + cv * V;
+        for (int t = pr; t < HW; t += 8) {
+            float v[V];
+            Vec16<T>::load(p + (size_t)t * C, v);
 #pragma unroll
-        for (int i = 0; i < V; ++i) s[i] += v[i];
+            for (int i = 0; i < V; ++i) s[i] += v[i];
+        }
     }
-    const float inv = 1.0f / (float)HW;
 #pragma unroll
-    for (int i = 0; i < V; ++i) s[i] *= inv;
-    Vec16<T>::store(y + (size_t)n * C + cv * V, s);
+    for (int i = 0; i < V; ++i) part[pr][threadIdx.x & 31][i] = s[i];
+    __syncthreads();
+    if (pr == 0 && cv < CV) {
+        const float inv = 1.0f / (float)HW;
+        float o[V];
+#pragma unroll
+        for (int i = 0; i < V; ++i) {
+            float t = 0.0f;
+            for (int r = 0; r < 8; ++r) t += part[r][threadIdx.x][i];
+            o[i] = t * inv;
+        }
+        Vec16<T>::store(y + (size_t)n * C + cv * V, o);
+    }
 }
 
 template <typename T>
@@ -207,9 +223,10 @@ hipError_t launch_maxpool(int dt, const void* x, void* y, int N, int H, int W, i
 
 hipError_t launch_gap(int dt, const void* x, void* y, int N, int HW, int C, hipStream_t s)
 {
-    const size_t total = (size_t)N * C / (16 / dtype_size(dt));
-    PPIPE_DISPATCH(dt, hipLaunchKernelGGL(gap_kernel<T>, dim3(blocks_for(total)), dim3(256),
-                                          0, s, (const T*)x, (T*)y, N, HW, C));
+    const int CV = C / (16 / dtype_size(dt));
+    const unsigned blocks = (unsigned)N * ((CV + 31) / 32);
+    PPIPE_DISPATCH(dt, hipLaunchKernelGGL(gap_kernel<T>, dim3(blocks), dim3(256), 0, s,
+                                          (const T*)x, (T*)y, N, HW, C));
     return hipGetLastError();
 }
 

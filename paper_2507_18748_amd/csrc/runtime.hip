@@ -18,6 +18,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -87,7 +88,7 @@ enum Kind { K_GEMM = 0, K_DW = 1, K_MAXPOOL = 2, K_GAP = 3 };
 enum { BUF_IN = -1, BUF_OUT = -2, BUF_NONE = -3 };
 
 struct Plan {
-    int cfg, splits, chunks_per_split, total_chunks;
+    int cfg, wk, splits, chunks_per_split, total_chunks, tiles_m, tiles_co, co_fastest;
 };
 
 struct Shape {
@@ -100,7 +101,7 @@ struct LayerRT {
     int index, op, src, res_src, act, k, stride, pad, groups;
     int H, W, C, Ho, Wo, Co;
     int kind;
-    bool generic = false, softmax = false;
+    bool generic = false, softmax = false, skinny_ok = false;
     int KH = 1, KW = 1, gstride = 1, gpad = 0, K = 0, Kpad = 0;
     size_t w_off = 0, scale_off = 0, bias_off = 0;
     void* w = nullptr;
@@ -127,7 +128,7 @@ struct ppipe_partition {
     std::vector<LayerRT> L;
     std::vector<void*> slots;
     std::vector<size_t> slot_bytes;
-    float* ws = nullptr;
+    float* ws = nullptr;          // split-K partials, then fp32 logits of a final FC + softmax
     size_t ws_bytes = 0;
     void* wblob = nullptr;
     size_t wbytes = 0;
@@ -138,28 +139,63 @@ struct ppipe_partition {
 
 namespace {
 
-Plan choose_plan(int M, int Co, int K, int dt)
+// Kernel plan of a GEMM-shaped layer at one batch: kernel family, tile
+// shape, waves per tile (skinny) and tile order.  Deterministic in (M, Co, K,
+// dtype, eligibility) so that the latency table, the benchmark and the
+// parity tests exercise the same launches.
+Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok)
 {
     auto tiles = [&](int cfg) {
         GemmCfgInfo c = gemm_cfg_info(cfg);
         return (int64_t)((M + c.bn - 1) / c.bn) * ((Co + c.bm - 1) / c.bm);
     };
-    int cfg;
-    if (M <= 32)
-        cfg = GEMM_64x16;
-    else if (tiles(GEMM_128x128) >= 256)
-        cfg = GEMM_128x128;
-    else
-        cfg = GEMM_64x64;
-    const int bk = gemm_bk(cfg, dt);
-    const int total = (K + bk - 1) / bk;
-    const int64_t t = tiles(cfg);
+    auto steps = [&](int cfg) { return (K + gemm_bk(cfg, dt) - 1) / gemm_bk(cfg, dt); };
+    int cfg = Co <= 64 && tiles(GEMM_64x128) >= 512 ? GEMM_64x128 : GEMM_64x64, wk = 0;
+    // Few tiles: split K until about two blocks per CU, keeping >= 2 stages
+    // per split (measured on MI355X: the per-block K loop is latency-bound, so
+    // short splits win even after the extra reduction pass).
     int splits = 1;
-    while (t * splits * 2 <= 512 && total / (splits * 2) >= 8 && splits * 2 <= 32)
-        splits *= 2;
-    const int cps = (total + splits - 1) / splits;
-    splits = (total + cps - 1) / cps;
-    return {cfg, splits, cps, total};
+    {
+        const int64_t t = tiles(cfg);
+        while (t * splits * 2 <= 512 && steps(cfg) / (splits * 2) >= 2 && splits < 32)
+            splits *= 2;
+    }
+    // PPIPE_GEMM_PLAN="cfg,waves,splits" forces one configuration on every
+    // eligible GEMM layer (tuning sweeps and kernel tests).
+    if (const char* env = std::getenv("PPIPE_GEMM_PLAN")) {
+        int fc = -1, fw = 0, fs = 1;
+        if (std::sscanf(env, "%d,%d,%d", &fc, &fw, &fs) >= 1 && fc >= 0 && fc < GEMM_NCFG) {
+            const bool sk = gemm_cfg_info(fc).skinny;
+            const bool wk_ok = fw == 4 || fw == 8 || (fw == 16 && fc == GEMM_SK_16x16);
+            if (!sk) {
+                cfg = fc;
+                wk = 0;
+                splits = std::max(1, std::min(fs, 64));
+            } else if (skinny_ok && wk_ok) {
+                cfg = fc;
+                wk = fw;
+                splits = 1;
+            }
+        }
+    }
+    const GemmCfgInfo c = gemm_cfg_info(cfg);
+    Plan p;
+    p.cfg = cfg;
+    p.wk = wk;
+    p.total_chunks = steps(cfg);
+    p.chunks_per_split = (p.total_chunks + splits - 1) / splits;
+    p.splits = (p.total_chunks + p.chunks_per_split - 1) / p.chunks_per_split;
+    p.tiles_m = (M + c.bn - 1) / c.bn;
+    p.tiles_co = (Co + c.bm - 1) / c.bm;
+    p.co_fastest = M > Co ? 1 : 0;   // keep the larger operand's slices on one XCD
+    return p;
+}
+
+// The scalar-gather variant applies to the LDS-staged kernel only; a layer
+// planned on the skinny kernel is always vector-loadable (skinny_ok).
+bool gather(const LayerRT& l, const Plan& p)
+{
+    return l.generic && !gemm_cfg_info(p.cfg).skinny;
 }
 
 const void* buf_ptr(const ppipe_partition* P, int id, const void* in, void* out)
@@ -180,8 +216,7 @@ struct LaunchHook {
 int layer_launches(const LayerRT& l, int batch)
 {
     if (l.kind != K_GEMM) return 1;
-    const Plan& p = l.plans[batch - 1];
-    return (l.softmax || p.splits > 1) ? 2 : 1;
+    return 1 + (l.plans[batch - 1].splits > 1 ? 1 : 0) + (l.softmax ? 1 : 0);
 }
 
 std::string launch_name(const ppipe_partition* P, const LayerRT& l, int batch, int launch)
@@ -189,11 +224,9 @@ std::string launch_name(const ppipe_partition* P, const LayerRT& l, int batch, i
     switch (l.kind) {
     case K_GEMM: {
         const Plan& p = l.plans[batch - 1];
-        if (launch == 0) {
-            std::string s = conv_gemm_name(P->dtype, p.cfg, l.generic);
-            return s;
-        }
-        return l.softmax ? splitk_softmax_name() : splitk_epilogue_name(P->dtype);
+        if (launch == 0) return conv_gemm_name(P->dtype, p.cfg, p.wk, gather(l, p));
+        if (launch == 1 && p.splits > 1) return splitk_reduce_name(P->dtype);
+        return softmax_rows_name();
     }
     case K_DW: return dwconv_name(P->dtype, l.k);
     case K_MAXPOOL: return maxpool_name(P->dtype);
@@ -201,31 +234,31 @@ std::string launch_name(const ppipe_partition* P, const LayerRT& l, int batch, i
     }
 }
 
-// Algorithmic work attributed to one launch: the GEMM launch owns the FLOPs,
-// input and weight bytes; a following reduction owns the output (+ residual).
+// Algorithmic work of one launch: FLOPs, and the layer's input, weight,
+// output and residual bytes each counted once.  When a layer takes several
+// launches the GEMM owns the FLOPs, input and weights, the last launch the
+// output (and residual); a split-K reduction between them owns nothing.
 void launch_work(const ppipe_partition* P, const LayerRT& l, int batch, int launch,
                  double* flops, double* bytes)
 {
     const double b = batch;
     const double out_bytes = b * (double)l.out_bytes_b1 *
                              (l.softmax ? 4.0 / dtype_size(P->dtype) : 1.0);
-    const double all = b * (l.in_bytes_b1 + l.res_bytes_b1) + out_bytes + l.param_bytes;
-    if (l.kind != K_GEMM || layer_launches(l, batch) == 1) {
+    const int n = layer_launches(l, batch);
+    const double in_w = b * l.in_bytes_b1 + l.param_bytes;
+    const double out_r = out_bytes + b * l.res_bytes_b1;
+    if (n == 1) {
         *flops = b * l.flops_b1;
-        *bytes = all;
+        *bytes = in_w + out_r;
         return;
     }
-    if (launch == 0) {
-        *flops = b * l.flops_b1;
-        *bytes = b * l.in_bytes_b1 + l.param_bytes;
-    } else {
-        *flops = 0;
-        *bytes = b * l.res_bytes_b1 + out_bytes;
-    }
+    *flops = launch == 0 ? b * l.flops_b1 : 0.0;
+    *bytes = launch == 0 ? in_w : (launch == n - 1 ? out_r : 0.0);
 }
 
+// Enqueue the launches of one layer; only >= 0 restricts to that launch.
 hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, const void* in,
-                         void* out, hipStream_t s, LaunchHook* hook)
+                         void* out, hipStream_t s, LaunchHook* hook, int only = -1)
 {
     const void* x = buf_ptr(P, l.in_buf, in, out);
     void* y = const_cast<void*>(buf_ptr(P, l.out_buf, in, out));
@@ -241,30 +274,41 @@ hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, 
         a.bias = l.bias;
         a.res = res;
         a.y = y;
+        a.M = batch * l.Ho * l.Wo;
         a.partial = P->ws;
+        a.logits = P->ws + (p.splits > 1 ? (size_t)p.splits * a.M * l.Co : 0);
         a.N = batch;
         a.H = l.H; a.W = l.W; a.C = l.C;
         a.Ho = l.Ho; a.Wo = l.Wo; a.Co = l.Co;
         a.KH = l.KH; a.KW = l.KW; a.stride = l.gstride; a.pad = l.gpad;
         a.K = l.K; a.Kpad = l.Kpad;
-        a.M = batch * l.Ho * l.Wo;
         a.act = l.act;
         a.total_chunks = p.total_chunks;
+        a.splits = p.splits;
         a.chunks_per_split = p.chunks_per_split;
-        const bool two = l.softmax || p.splits > 1;
-        a.out_mode = two ? 1 : 0;
-        if (hook) hook->before(l, 0, s);
-        e = launch_conv_gemm(P->dtype, p.cfg, l.generic, a, p.splits, s);
-        if (hook) hook->after(l, 0, s);
-        if (e != hipSuccess || !two)
-            return e;
-        if (hook) hook->before(l, 1, s);
-        if (l.softmax)
-            e = launch_splitk_softmax(P->ws, p.splits, a.M, l.Co, l.bias, (float*)y, s);
-        else
-            e = launch_splitk_epilogue(P->dtype, P->ws, p.splits, a.M, l.Co, l.scale, l.bias,
-                                       res, l.act, y, s);
-        if (hook) hook->after(l, 1, s);
+        a.tiles_m = p.tiles_m;
+        a.tiles_co = p.tiles_co;
+        a.co_fastest = p.co_fastest;
+        a.softmax = l.softmax ? 1 : 0;
+        if (only <= 0) {
+            if (hook) hook->before(l, 0, s);
+            e = launch_conv_gemm(P->dtype, p.cfg, p.wk, gather(l, p), a, s);
+            if (hook) hook->after(l, 0, s);
+        }
+        int next = 1;
+        if (e == hipSuccess && p.splits > 1) {
+            if (only < 0 || only == next) {
+                if (hook) hook->before(l, next, s);
+                e = launch_splitk_reduce(P->dtype, a, s);
+                if (hook) hook->after(l, next, s);
+            }
+            ++next;
+        }
+        if (e == hipSuccess && l.softmax && (only < 0 || only == next)) {
+            if (hook) hook->before(l, next, s);
+            e = launch_softmax_rows(a.logits, a.M, l.Co, (float*)y, s);
+            if (hook) hook->after(l, next, s);
+        }
         return e;
     }
     case K_DW:
@@ -331,6 +375,7 @@ void release(ppipe_partition* P)
     for (void* s : P->slots) (void)hipFree(s);
     P->slots.clear();
     if (P->ws) (void)hipFree(P->ws);
+
     if (P->wblob) (void)hipFree(P->wblob);
     if (P->cap_stream) (void)hipStreamDestroy(P->cap_stream);
     P->ws = nullptr;
@@ -472,12 +517,21 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
             l.Kpad = (l.K + 63) / 64 * 64;
             const int bk_min = gemm_bk(GEMM_128x128, dt);   // every config uses the same BK
             l.generic = !(x.c % epv == 0 && (l.KH * l.KW == 1 || x.c % bk_min == 0));
+            // skinny kernel: each 64-byte K step lies in one (kh, kw) tap
+            l.skinny_ok = x.c % epv == 0 && (l.KH * l.KW == 1 || x.c % (4 * epv) == 0);
             if (l.generic && l.Kpad > GEMM_KTAB_MAX)
                 return fail(PPIPE_E_UNSUPPORTED, who + ": reduction length " +
                                                      std::to_string(l.K) + " with C = " +
                                                      std::to_string(x.c) + " is not supported");
             if (!ld.weight)
                 return fail(PPIPE_E_INVALID, who + ": missing weight");
+            // operands are addressed with 32-bit byte offsets (buffer loads)
+            if ((double)P->max_batch * x.c * x.h * x.w * esz >= 2147483648.0 ||
+                (double)o.c * ((l.K + 63) / 64 * 64) * esz >= 2147483648.0)
+                return fail(PPIPE_E_UNSUPPORTED, who + ": input or weights reach 2 GiB at "
+                                                       "max_batch");
+            if (l.KH > 32 || l.KW > 32)
+                return fail(PPIPE_E_UNSUPPORTED, who + ": window larger than 32");
             l.flops_b1 = 2.0 * o.c * o.h * o.w * (double)l.K;
             l.param_bytes = (double)o.c * l.K * esz + 8.0 * o.c;
         } else if (ld.op == PPIPE_OP_MAXPOOL) {
@@ -599,17 +653,19 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
         l.out_buf = slot;
     }
 
-    // ---- kernel plans for every batch, split-K workspace ----
+    // ---- kernel plans for every batch, logits workspace ----
     size_t ws = 0;
     for (LayerRT& l : P->L) {
         if (l.kind != K_GEMM) continue;
         l.plans.resize(P->max_batch);
         for (int b = 1; b <= P->max_batch; ++b) {
             const int M = b * l.Ho * l.Wo;
-            Plan p = choose_plan(M, l.Co, l.K, dt);
+            const Plan p = choose_plan(M, l.Co, l.K, dt, l.skinny_ok);
             l.plans[b - 1] = p;
-            if (p.splits > 1 || l.softmax)
-                ws = std::max(ws, (size_t)p.splits * M * l.Co * sizeof(float));
+            size_t need = 0;
+            if (p.splits > 1) need += (size_t)p.splits * M * l.Co;
+            if (l.softmax) need += (size_t)M * l.Co;
+            ws = std::max(ws, need * sizeof(float));
         }
     }
     P->ws_bytes = ws;
@@ -646,25 +702,11 @@ int allocate(ppipe_partition* P)
         e = hipMalloc((void**)&P->ws, P->ws_bytes);
         if (e != hipSuccess) return fail(PPIPE_E_NOMEM, hip_msg("hipMalloc(split-K)", e));
     }
+
     e = hipStreamCreateWithFlags(&P->cap_stream, hipStreamNonBlocking);
     if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipStreamCreate", e));
     return PPIPE_OK;
 }
-
-// Event hook for per-launch timing.
-struct EventHook : LaunchHook {
-    std::vector<hipEvent_t> ev;   // 2 per launch
-    size_t next = 0;
-    hipError_t err = hipSuccess;
-    void before(const LayerRT&, int, hipStream_t s) override
-    {
-        if (err == hipSuccess) err = hipEventRecord(ev[next++], s);
-    }
-    void after(const LayerRT&, int, hipStream_t s) override
-    {
-        if (err == hipSuccess) err = hipEventRecord(ev[next++], s);
-    }
-};
 
 struct ProfileBuffers {
     void* in = nullptr;
@@ -694,6 +736,45 @@ int setup_profile(ppipe_partition* P, ProfileBuffers& pb)
     return PPIPE_OK;
 }
 
+}  // namespace
+
+// Timing method shared by both profilers: a layer (or one launch) is
+// enqueued `reps` times back to back between two events on the profiling
+// stream; the per-launch time is the elapsed time / reps.  Repeating the
+// same launch amortises the event and dispatch overhead that a pair of
+// events around one short kernel would add.  Three such trials are taken
+// and the median (and minimum) reported.
+namespace {
+constexpr int PROFILE_TRIALS = 3;
+
+struct Events {
+    hipEvent_t a = nullptr, b = nullptr;
+    ~Events()
+    {
+        if (a) (void)hipEventDestroy(a);
+        if (b) (void)hipEventDestroy(b);
+    }
+    hipError_t make()
+    {
+        hipError_t e = hipEventCreate(&a);
+        return e == hipSuccess ? hipEventCreate(&b) : e;
+    }
+};
+
+template <typename F>
+hipError_t time_reps(hipStream_t s, Events& ev, int reps, F&& enqueue, std::vector<float>& us)
+{
+    hipError_t e = hipEventRecord(ev.a, s);
+    for (int r = 0; r < reps && e == hipSuccess; ++r)
+        e = enqueue();
+    if (e == hipSuccess) e = hipEventRecord(ev.b, s);
+    if (e == hipSuccess) e = hipEventSynchronize(ev.b);
+    if (e != hipSuccess) return e;
+    float ms = 0;
+    e = hipEventElapsedTime(&ms, ev.a, ev.b);
+    us.push_back(ms * 1000.0f / (float)reps);
+    return e;
+}
 }  // namespace
 
 extern "C" {
@@ -810,51 +891,41 @@ int ppipe_profile_layers(ppipe_partition* h, const int32_t* batch_sizes, int32_t
     if (rc != PPIPE_OK) return rc;
     ProfileBuffers pb;
     if ((rc = setup_profile(h, pb)) != PPIPE_OK) return rc;
+    Events ev;
+    hipError_t e = ev.make();
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipEventCreate", e));
     const int nl = (int)h->L.size();
-    std::vector<hipEvent_t> ev(nl + 1);
-    for (auto& x : ev) {
-        hipError_t e = hipEventCreate(&x);
-        if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipEventCreate", e));
-    }
-    struct EvGuard {
-        std::vector<hipEvent_t>& v;
-        ~EvGuard() { for (auto x : v) if (x) (void)hipEventDestroy(x); }
-    } guard{ev};
     for (int j = 0; j < n_batches; ++j) {
         const int b = batch_sizes[j];
-        hipError_t e = hipSuccess;
         for (int w = 0; w < warmup && e == hipSuccess; ++w)
             e = enqueue_all(h, b, pb.in, pb.out, pb.s, nullptr);
         if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("kernel launch", e));
-        std::vector<std::vector<float>> per(nl);
-        std::vector<float> whole;
-        for (int r = 0; r < reps; ++r) {
-            e = hipEventRecord(ev[0], pb.s);
-            for (int i = 0; i < nl && e == hipSuccess; ++i) {
-                e = enqueue_layer(h, h->L[i], b, pb.in, pb.out, pb.s, nullptr);
-                if (e == hipSuccess) e = hipEventRecord(ev[i + 1], pb.s);
-            }
-            if (e == hipSuccess) e = hipEventSynchronize(ev[nl]);
+        for (int i = 0; i < nl; ++i) {
+            std::vector<float> t;
+            for (int k = 0; k < PROFILE_TRIALS && e == hipSuccess; ++k)
+                e = time_reps(pb.s, ev, reps, [&] {
+                    return enqueue_layer(h, h->L[i], b, pb.in, pb.out, pb.s, nullptr);
+                }, t);
             if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("profile run", e));
-            for (int i = 0; i < nl; ++i) {
-                float ms = 0;
-                (void)hipEventElapsedTime(&ms, ev[i], ev[i + 1]);
-                per[i].push_back(ms * 1000.0f);
-            }
+            if (out_us) out_us[(size_t)i * n_batches + j] = median_of(t);
         }
-        for (int r = 0; r < reps; ++r) {
-            e = hipEventRecord(ev[0], pb.s);
-            if (e == hipSuccess) e = enqueue_all(h, b, pb.in, pb.out, pb.s, nullptr);
-            if (e == hipSuccess) e = hipEventRecord(ev[1], pb.s);
-            if (e == hipSuccess) e = hipEventSynchronize(ev[1]);
-            if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("profile run", e));
-            float ms = 0;
-            (void)hipEventElapsedTime(&ms, ev[0], ev[1]);
-            whole.push_back(ms * 1000.0f);
+        // whole range as run() executes it: one captured graph replayed
+        hipGraph_t g = nullptr;
+        hipGraphExec_t x = nullptr;
+        e = hipStreamBeginCapture(pb.s, hipStreamCaptureModeThreadLocal);
+        if (e == hipSuccess) {
+            hipError_t le = enqueue_all(h, b, pb.in, pb.out, pb.s, nullptr);
+            e = hipStreamEndCapture(pb.s, &g);
+            if (e == hipSuccess) e = le;
         }
-        if (out_us)
-            for (int i = 0; i < nl; ++i) out_us[(size_t)i * n_batches + j] = median_of(per[i]);
-        if (out_partition_us) out_partition_us[j] = median_of(whole);
+        if (e == hipSuccess) e = hipGraphInstantiate(&x, g, nullptr, nullptr, 0);
+        std::vector<float> t;
+        for (int k = 0; k < PROFILE_TRIALS && e == hipSuccess; ++k)
+            e = time_reps(pb.s, ev, reps, [&] { return hipGraphLaunch(x, pb.s); }, t);
+        if (x) (void)hipGraphExecDestroy(x);
+        if (g) (void)hipGraphDestroy(g);
+        if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("profile graph run", e));
+        if (out_partition_us) out_partition_us[j] = median_of(t);
     }
     return PPIPE_OK;
 }
@@ -872,36 +943,21 @@ int ppipe_profile_kernels(ppipe_partition* h, int32_t batch, int32_t warmup, int
     *count = nlaunch;
     ProfileBuffers pb;
     if ((rc = setup_profile(h, pb)) != PPIPE_OK) return rc;
-    EventHook hook;
-    hook.ev.resize(2 * (size_t)nlaunch);
-    for (auto& x : hook.ev) {
-        hipError_t e = hipEventCreate(&x);
-        if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipEventCreate", e));
-    }
-    struct EvGuard {
-        std::vector<hipEvent_t>& v;
-        ~EvGuard() { for (auto x : v) if (x) (void)hipEventDestroy(x); }
-    } guard{hook.ev};
-    hipError_t e = hipSuccess;
+    Events ev;
+    hipError_t e = ev.make();
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipEventCreate", e));
     for (int w = 0; w < warmup && e == hipSuccess; ++w)
         e = enqueue_all(h, batch, pb.in, pb.out, pb.s, nullptr);
     if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("kernel launch", e));
-    std::vector<std::vector<float>> t(nlaunch);
-    for (int r = 0; r < reps; ++r) {
-        hook.next = 0;
-        e = enqueue_all(h, batch, pb.in, pb.out, pb.s, &hook);
-        if (e == hipSuccess) e = hook.err;
-        if (e == hipSuccess) e = hipEventSynchronize(hook.ev.back());
-        if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("profile run", e));
-        for (int k = 0; k < nlaunch; ++k) {
-            float ms = 0;
-            (void)hipEventElapsedTime(&ms, hook.ev[2 * k], hook.ev[2 * k + 1]);
-            t[k].push_back(ms * 1000.0f);
-        }
-    }
     int k = 0;
     for (const LayerRT& l : h->L) {
         for (int j = 0; j < layer_launches(l, batch); ++j, ++k) {
+            std::vector<float> t;
+            for (int q = 0; q < PROFILE_TRIALS && e == hipSuccess; ++q)
+                e = time_reps(pb.s, ev, reps, [&] {
+                    return enqueue_layer(h, l, batch, pb.in, pb.out, pb.s, nullptr, j);
+                }, t);
+            if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("profile run", e));
             if (!records || k >= capacity) continue;
             ppipe_kernel_record& rec = records[k];
             std::memset(&rec, 0, sizeof(rec));
@@ -911,11 +967,10 @@ int ppipe_profile_kernels(ppipe_partition* h, int32_t batch, int32_t warmup, int
                           launch_name(h, l, batch, j).c_str());
             launch_work(h, l, batch, j, &rec.flops, &rec.bytes);
             double sum = 0;
-            float mn = t[k].empty() ? 0.f : t[k][0];
-            for (float v : t[k]) { sum += v; mn = std::min(mn, v); }
-            rec.mean_us = (float)(sum / std::max<size_t>(1, t[k].size()));
-            rec.median_us = median_of(t[k]);
-            rec.min_us = mn;
+            for (float v : t) sum += v;
+            rec.mean_us = (float)(sum / t.size());
+            rec.median_us = median_of(t);
+            rec.min_us = *std::min_element(t.begin(), t.end());
         }
     }
     return PPIPE_OK;
@@ -962,7 +1017,8 @@ int ppipe_layer_info(const ppipe_partition* h, int32_t index, int32_t batch,
     std::string k = launch_name(h, l, batch, 0);
     if (l.kind == K_GEMM) {
         const Plan& p = l.plans[batch - 1];
-        k += " splits=" + std::to_string(p.splits);
+        k += " tiles=" + std::to_string(p.tiles_m * p.tiles_co) + " splits=" +
+             std::to_string(p.splits);
     }
     std::snprintf(info->kernel, sizeof(info->kernel), "%s", k.c_str());
     return PPIPE_OK;

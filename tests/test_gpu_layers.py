@@ -144,3 +144,71 @@ def test_fc_large_k_small_batch(dtype):
     m = make((4096, 1, 1), [dict(name="fc", op="fc", src=-1, c_in=4096, c_out=1000,
                                  act="relu", bias=True)])
     check(m, dtype, 1)
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16", "f32"])
+def test_conv_lds_64x64(dtype):
+    # M = 10*32*32 = 10240, Co = 64: the LDS-staged 64x64 configuration
+    check(make((64, 32, 32), [conv("c", -1, 64, 64, 3, 1, 1)]), dtype, 10)
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+def test_conv_lds_64x128(dtype):
+    # M = 5*64*64 = 20480, Co = 64: the 64 x 128 configuration
+    check(make((64, 64, 64), [conv("c", -1, 64, 64, 3, 1, 1)]), dtype, 5)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_skinny_32x32(dtype):
+    # M = 4*16*16 = 1024, Co = 256: 32x32 skinny tiles
+    check(make((64, 16, 16), [conv("c", -1, 64, 256, act="none")]), dtype, 4)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_skinny_32x16(dtype):
+    # the ResNet-50 layer4 3x3 shape: M = 8*7*7 = 392, Co = 512, K = 4608
+    check(make((512, 7, 7), [conv("c", -1, 512, 512, 3, 1, 1)]), dtype, 8)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_skinny_16x32(dtype):
+    # a 4096-wide FC at batch 2 (the VGG classifier shape)
+    m = make((512, 1, 1), [dict(name="fc", op="fc", src=-1, c_in=512, c_out=4096,
+                                act="relu", bias=True)])
+    check(m, dtype, 2, kind="relu_normal")
+
+
+FORCED = [  # (configuration id, waves, splits): every kernel variant the planner can emit
+    ("0,0,1", "conv_gemm<", "128x128"), ("0,0,4", "conv_gemm<", "128x128"),
+    ("1,0,1", "conv_gemm<", "64x64"), ("1,0,3", "conv_gemm<", "64x64"),
+    ("2,0,1", "conv_gemm<", "64x128"), ("2,0,2", "conv_gemm<", "64x128"),
+    ("3,4", "conv_gemm_skinny<", "32x32"), ("3,8", "conv_gemm_skinny<", "32x32"),
+    ("4,4", "conv_gemm_skinny<", "32x16"), ("4,8", "conv_gemm_skinny<", "32x16"),
+    ("5,4", "conv_gemm_skinny<", "16x32"), ("5,8", "conv_gemm_skinny<", "16x32"),
+    ("6,4", "conv_gemm_skinny<", "16x16"), ("6,8", "conv_gemm_skinny<", "16x16"),
+    ("6,16", "conv_gemm_skinny<", "16x16"),
+]
+FORCED_SHAPES = {  # ragged M and Co, padded 3x3 taps, a 1x1 with a K tail, an FC + softmax
+    "3x3": ((64, 13, 13), [conv("c", -1, 64, 100, 3, 1, 1)], 3, "normal"),
+    "1x1": ((24, 9, 9), [conv("c", -1, 24, 36, act="relu6")], 2, "normal"),
+    "fc": ((96, 3, 3), [dict(name="fc", op="fc_softmax", src=-1, c_in=96 * 9, c_out=200,
+                             bias=True)], 5, "relu_normal"),
+}
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("shape", list(FORCED_SHAPES))
+@pytest.mark.parametrize("plan,family,tile", FORCED)
+def test_forced_gemm_configuration(monkeypatch, plan, family, tile, shape, dtype):
+    """Every tile configuration, wave count and split count against the oracle
+    (forced through the planner override)."""
+    from paper_2507_18748_amd import Partition
+    in_chw, specs, batch, kind = FORCED_SHAPES[shape]
+    monkeypatch.setenv("PPIPE_GEMM_PLAN", plan)
+    m = make(in_chw, specs)
+    with Partition(m.layers, W.model_params(m, 0, dtype), in_chw, 0, 1, dtype,
+                   max_batch=batch) as part:
+        k = part.layer_info(0, batch)["kernel"]
+    assert k.startswith(family) and tile in k, (plan, k)
+    tol = {"f32": 1e-5, "bf16": 2.0 ** -7}[dtype] if shape != "fc" else 2e-2
+    check(m, dtype, batch, kind=kind, tol=tol)
