@@ -68,6 +68,73 @@ def cpu_baseline(wl, m, P, target_s):
                       f"{el:.1f} s wall"}
 
 
+def parse_batches(spec):
+    if "-" in spec and "," not in spec:
+        lo, hi = (int(v) for v in spec.split("-"))
+        return list(range(lo, hi + 1))
+    return [int(v) for v in spec.split(",")]
+
+
+def latency_table(args):
+    """Per-layer latency table L[i][b] (microseconds, median of back-to-back
+    repetitions) of the workload's partition, with the feature-map size S_i,
+    each layer's algorithmic work and roofline position, and the measured
+    whole-partition latency next to the sum of its layers (the paper's
+    planner assumes partition latency = sum of layer latencies)."""
+    import numpy as np
+    import torch
+    import workloads as W
+    from paper_2507_18748_amd import Partition
+    wl = W.workload(args.workload)
+    batches = parse_batches(args.batches)
+    m = wl.build_model()
+    P = wl.params(m)
+    torch.cuda.set_device(0)
+    part = Partition(m.layers, P, (m.in_c, m.in_h, m.in_w), wl.begin, wl.end, wl.dtype,
+                     max_batch=max(batches))
+    peak_f = PEAK_MFMA_TFLOPS[wl.dtype] * 1e12
+    peak_b = PEAK_HBM_GBS * 1e9
+    rows = []
+    table = np.zeros((wl.end - wl.begin, len(batches)))
+    whole = np.zeros(len(batches))
+    chunk = 8
+    for c0 in range(0, len(batches), chunk):
+        bs = batches[c0:c0 + chunk]
+        t, w = part.profile_layers(bs, warmup=3, reps=args.profile_reps)
+        table[:, c0:c0 + len(bs)] = t
+        whole[c0:c0 + len(bs)] = w
+        print(f"[table] batches {bs[0]}..{bs[-1]} done", file=sys.stderr, flush=True)
+    for i in range(wl.begin, wl.end):
+        info = part.layer_info(i, batches[-1])
+        row = {"layer": i, "name": m.layers[i].name, "op": m.layers[i].op,
+               "S_i_bytes": info["out_bytes_b1"], "out_chw": [info["out_c"], info["out_h"], info["out_w"]],
+               "us": {}, "roofline_frac": {}, "bound": {}}
+        for j, b in enumerate(batches):
+            li = part.layer_info(i, b)
+            fl = b * li["flops_b1"]
+            by = b * li["act_bytes_b1"] + li["param_bytes"]
+            t_roof = max(fl / peak_f, by / peak_b)
+            us = float(table[i - wl.begin, j])
+            row["us"][b] = us
+            row["roofline_frac"][b] = t_roof * 1e6 / us if us > 0 else None
+            row["bound"][b] = "mfma" if fl / peak_f >= by / peak_b else "hbm"
+        row["kernel_at_max_batch"] = info["kernel"]
+        rows.append(row)
+    out = {"workload": wl.name, "description": wl.description, "dtype": wl.dtype,
+           "layers": [wl.begin, wl.end], "batches": batches,
+           "partition_us": {b: float(whole[j]) for j, b in enumerate(batches)},
+           "sum_of_layers_us": {b: float(table[:, j].sum()) for j, b in enumerate(batches)},
+           "images_per_s": {b: b / (whole[j] * 1e-6) for j, b in enumerate(batches)},
+           "method": "median of 3 trials of back-to-back repetitions between HIP events; "
+                     "partition = one captured HIP graph replayed",
+           "rows": rows}
+    with open(args.table, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps({"table": args.table, "workload": wl.name, "batches": len(batches),
+                      "partition_us": out["partition_us"]}))
+    part.close()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -79,6 +146,14 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="oracle sample length for cpu_baseline (0 disables)")
     ap.add_argument("--profile-reps", type=int, default=50)
+    ap.add_argument("--table", metavar="OUT.json", default=None,
+                    help="instead of the benchmark, write the per-layer latency table of the "
+                         "workload (median us per layer at each --batches size) with S_i and "
+                         "per-layer roofline fractions")
+    ap.add_argument("--batches", default="1-64",
+                    help="batch sizes for --table: '1-64', or a comma list")
+    ap.add_argument("--kernels", metavar="OUT.json", default=None,
+                    help="also write every launch's timing record of the benchmark batch")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB mebibytes 10 times "
                          "(reference for the HBM byte counters) and exit")
@@ -103,6 +178,9 @@ def main():
         return
     import workloads as W
     from paper_2507_18748_amd import Partition
+
+    if args.table:
+        return latency_table(args)
 
     wl = W.workload(args.workload)
     if args.batch:
@@ -145,6 +223,9 @@ def main():
 
     recs = part.profile_kernels(wl.batch, warmup=10, reps=args.profile_reps)
     roof = roofline(recs, wl.dtype)
+    if args.kernels:
+        with open(args.kernels, "w") as f:
+            json.dump(recs, f, indent=1)
     print(f"[bench] dominant kernel {roof['kernel']}: {roof['achieved']:.1f} {roof['unit']} "
           f"({roof['frac'] * 100:.1f}% of peak)", file=sys.stderr, flush=True)
 

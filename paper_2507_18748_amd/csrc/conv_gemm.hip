@@ -189,15 +189,6 @@ __device__ __forceinline__ uint4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t o
 {
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
-template <typename T>
-__device__ __forceinline__ T buf_load_elem(__amdgpu_buffer_rsrc_t r, uint32_t off)
-{
-    if constexpr (sizeof(T) == 4)
-        return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
-    else
-        return __builtin_bit_cast(T, __builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0));
-}
-
 // Position of a K step in (kh, kw, ci) order, wave-uniform, advanced by a
 // fixed number of channels; steps never straddle a tap (C is a multiple of the
 // step, or the window is 1x1 and the tail is cut by the channel test).
@@ -249,7 +240,12 @@ __device__ __forceinline__ PixelRow pixel_row(const ConvGemmArgs& a, int m, int 
 }
 
 // LDS-staged implicit GEMM for layers with many output pixels.
-template <typename T, int BM, int BN, int WM, int WN, int KV, int DEPTH, bool GENERIC>
+// TAPV: the channel count is a multiple of the vector width but not of the
+// stage, so each 16-byte vector of a stage may sit in a different (kh, kw)
+// tap; a per-block table in LDS maps vector index -> (kh, kw, ci).  Layers
+// with fewer channels than a vector (3-channel stems) get their channels
+// zero-padded by a prologue kernel and take this path.
+template <typename T, int BM, int BN, int WM, int WN, int KV, int DEPTH, bool TAPV>
 __global__ void __launch_bounds__(WM * WN * 64)
 conv_gemm_kernel(ConvGemmArgs a)
 {
@@ -263,16 +259,13 @@ conv_gemm_kernel(ConvGemmArgs a)
     constexpr int A_VECS = BM * KV, B_VECS = BN * KV;
     constexpr int A_PER = (A_VECS + NT - 1) / NT;
     constexpr int B_PER = (B_VECS + NT - 1) / NT;
-    constexpr int B_ELEMS = BN * BK;
-    constexpr int BE_PER = (B_ELEMS + NT - 1) / NT;
     constexpr int STAGE = (BM + BN) * ROW;
-    constexpr int RB = GENERIC ? 1 : B_PER, RBE = GENERIC ? BE_PER : 1;
     static_assert(KV % 4 == 0, "a stage holds whole 64-byte MFMA k-steps");
     static_assert(FM >= 1 && FN >= 1 && WTM % 16 == 0 && WTN % 16 == 0, "wave tile");
     static_assert(DEPTH == 2, "the LDS pipeline keeps two register sets in flight");
 
     __shared__ __attribute__((aligned(16))) unsigned char smem[2 * STAGE];
-    __shared__ int ktab[GENERIC ? GEMM_KTAB_MAX : 1];
+    __shared__ int vtab[TAPV ? GEMM_VTAB_MAX : 1];
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
@@ -285,15 +278,17 @@ conv_gemm_kernel(ConvGemmArgs a)
     const auto wsrc = make_rsrc(a.w, (uint32_t)a.Co * a.Kpad * ESZ);
     const auto xsrc = make_rsrc(a.x, (uint32_t)a.N * a.H * a.W * a.C * ESZ);
 
-    if constexpr (GENERIC) {
-        for (int k = tid; k < a.Kpad && k < GEMM_KTAB_MAX; k += NT) {
-            int t = -1;
+    if constexpr (TAPV) {
+        // vector q covers k = [q * EPV, q * EPV + EPV): one tap, channels ci..ci+EPV
+        for (int q = tid; q < a.Kpad / EPV && q < GEMM_VTAB_MAX; q += NT) {
+            int e = -1;
+            const int k = q * EPV;
             if (k < a.K) {
-                int tap = k / a.C, ci = k - tap * a.C;
-                int kh = tap / a.KW, kw = tap - kh * a.KW;
-                t = kh | (kw << 8) | (ci << 16);
+                const int tap = k / a.C, ci = k - tap * a.C;
+                const int kh = tap / a.KW, kw = tap - kh * a.KW;
+                e = kh | (kw << 8) | (ci << 16);
             }
-            ktab[k] = t;
+            vtab[q] = e;
         }
         __syncthreads();
     }
@@ -308,41 +303,34 @@ conv_gemm_kernel(ConvGemmArgs a)
         a_off[i] = ok ? (uint32_t)(((co0 + row) * a.Kpad + kv * EPV) * ESZ) : OOB;
         a_lds[i] = row * ROW + kv * 16;
     }
-    constexpr int BROWS = GENERIC ? BE_PER : B_PER;
-    PixelRow b_px[BROWS];
-    int b_k[BROWS], b_lds[BROWS];
+    PixelRow b_px[B_PER];
+    int b_k[B_PER], b_lds[B_PER];
 #pragma unroll
-    for (int i = 0; i < BROWS; ++i) {
-        const int v = tid + i * NT;
-        const int r = GENERIC ? v / BK : v / KV;
-        const int kk = GENERIC ? v % BK : v % KV;   // k column (gather) or 16-byte vector
-        const bool inrange = v < (GENERIC ? B_ELEMS : B_VECS);
-        b_px[i] = pixel_row(a, inrange ? m0 + r : a.M, ESZ);
-        b_k[i] = kk;
-        b_lds[i] = BM * ROW + r * ROW + (GENERIC ? kk * ESZ : kk * 16);
+    for (int i = 0; i < B_PER; ++i) {
+        const int v = tid + i * NT, r = v / KV, kv = v % KV;
+        b_px[i] = pixel_row(a, v < B_VECS ? m0 + r : a.M, ESZ);
+        b_k[i] = kv;
+        b_lds[i] = BM * ROW + r * ROW + kv * 16;
     }
 
     // register ring: two sets, DEPTH stages in flight
-    uint4 ra0[A_PER], ra1[A_PER], rb0[RB], rb1[RB];
-    T re0[RBE], re1[RBE];
+    uint4 ra0[A_PER], ra1[A_PER], rb0[B_PER], rb1[B_PER];
     TapCursor cur;              // (kh, kw, ci) of the next stage to load
     int lst = kc_begin;         // its stage index
     cur.start(kc_begin * BK, a.C, a.KW);
 
-    auto load_stage = [&](uint4 (&sa)[A_PER], uint4 (&sb)[RB], T (&se)[RBE]) {
+    auto load_stage = [&](uint4 (&sa)[A_PER], uint4 (&sb)[B_PER]) {
         const uint32_t k0b = (uint32_t)(lst * BK * ESZ);
 #pragma unroll
         for (int i = 0; i < A_PER; ++i)
             sa[i] = buf_load16(wsrc, a_off[i] + k0b);
-        if constexpr (GENERIC) {
-            const int k0 = lst * BK;
+        if constexpr (TAPV) {
 #pragma unroll
-            for (int i = 0; i < BE_PER; ++i) {
-                const int k = k0 + b_k[i];
-                const int t = k < a.K ? ktab[k] : 0;
-                const int kh = t & 0xff, kw = (t >> 8) & 0xff, ci = t >> 16;
-                const bool ok = k < a.K && ((b_px[i].hmask >> kh) & (b_px[i].wmask >> kw) & 1u);
-                se[i] = buf_load_elem<T>(
+            for (int i = 0; i < B_PER; ++i) {
+                const int e = vtab[lst * KV + b_k[i]];
+                const int kh = e & 0xff, kw = (e >> 8) & 0xff, ci = e >> 16;
+                const bool ok = e >= 0 && ((b_px[i].hmask >> kh) & (b_px[i].wmask >> kw) & 1u);
+                sb[i] = buf_load16(
                     xsrc, ok ? (uint32_t)(b_px[i].off + ((kh * a.W + kw) * a.C + ci) * ESZ) : OOB);
             }
         } else {
@@ -360,23 +348,15 @@ conv_gemm_kernel(ConvGemmArgs a)
             cur.advance(BK, a.C, a.KW);
         }
     };
-    auto store_stage = [&](unsigned char* S, const uint4 (&sa)[A_PER], const uint4 (&sb)[RB],
-                           const T (&se)[RBE]) {
+    auto store_stage = [&](unsigned char* S, const uint4 (&sa)[A_PER], const uint4 (&sb)[B_PER]) {
 #pragma unroll
         for (int i = 0; i < A_PER; ++i)
             if (tid + i * NT < A_VECS)
                 *(uint4*)(S + a_lds[i]) = sa[i];
-        if constexpr (GENERIC) {
 #pragma unroll
-            for (int i = 0; i < BE_PER; ++i)
-                if (tid + i * NT < B_ELEMS)
-                    *(T*)(S + b_lds[i]) = se[i];
-        } else {
-#pragma unroll
-            for (int i = 0; i < B_PER; ++i)
-                if (tid + i * NT < B_VECS)
-                    *(uint4*)(S + b_lds[i]) = sb[i];
-        }
+        for (int i = 0; i < B_PER; ++i)
+            if (tid + i * NT < B_VECS)
+                *(uint4*)(S + b_lds[i]) = sb[i];
     };
 
     floatx4 acc[FM][FN];
@@ -398,9 +378,9 @@ conv_gemm_kernel(ConvGemmArgs a)
     // (it went to LDS last step) with stage s + 2, run the MFMAs on LDS buffer
     // s & 1, then move the other set (stage s + 1) into the other LDS buffer.
     // A macro over two named sets keeps every register index a constant.
-#define PPIPE_STEP(s, A0, B0, E0, A1, B1, E1)                                                    \
+#define PPIPE_STEP(s, A0, B0, A1, B1)                                                            \
     do {                                                                                          \
-        load_stage(A0, B0, E0);                                                                   \
+        load_stage(A0, B0);                                                                       \
         const unsigned char* S = smem + ((s) & 1) * STAGE;                                        \
         _Pragma("unroll") for (int ks = 0; ks < KV / 4; ++ks) {                                   \
             uint4 af[FM], bf[FN];                                                                 \
@@ -413,18 +393,18 @@ conv_gemm_kernel(ConvGemmArgs a)
                     Mfma<T>::step(af[i], bf[j], acc[i][j]);                                       \
         }                                                                                         \
         if ((s) + 1 < nst)                                                                        \
-            store_stage(smem + (((s) + 1) & 1) * STAGE, A1, B1, E1);                              \
+            store_stage(smem + (((s) + 1) & 1) * STAGE, A1, B1);                                  \
         __syncthreads();                                                                          \
     } while (0)
     if (nst > 0) {
-        load_stage(ra0, rb0, re0);
-        load_stage(ra1, rb1, re1);
-        store_stage(smem, ra0, rb0, re0);
+        load_stage(ra0, rb0);
+        load_stage(ra1, rb1);
+        store_stage(smem, ra0, rb0);
         __syncthreads();
         for (int s0 = 0; s0 < nst; s0 += 2) {
-            PPIPE_STEP(s0, ra0, rb0, re0, ra1, rb1, re1);
+            PPIPE_STEP(s0, ra0, rb0, ra1, rb1);
             if (s0 + 1 < nst)
-                PPIPE_STEP(s0 + 1, ra1, rb1, re1, ra0, rb0, re0);
+                PPIPE_STEP(s0 + 1, ra1, rb1, ra0, rb0);
         }
     }
 #undef PPIPE_STEP
@@ -625,11 +605,11 @@ GemmCfgInfo gemm_cfg_info(int cfg)
 }
 
 template <typename T, int BM, int BN, int WM, int WN, int KV, int DEPTH>
-static hipError_t launch_lds(bool generic, const ConvGemmArgs& a, hipStream_t s)
+static hipError_t launch_lds(bool tapv, const ConvGemmArgs& a, hipStream_t s)
 {
     dim3 grid((unsigned)(a.tiles_m * a.tiles_co * a.splits));
     dim3 block(WM * WN * 64);
-    if (generic)
+    if (tapv)
         hipLaunchKernelGGL((conv_gemm_kernel<T, BM, BN, WM, WN, KV, DEPTH, true>), grid, block,
                            0, s, a);
     else
@@ -662,15 +642,15 @@ static hipError_t launch_skinny(int wk, const ConvGemmArgs& a, hipStream_t s)
 }
 
 template <typename T>
-static hipError_t launch_cfg(int cfg, int wk, bool generic, const ConvGemmArgs& a,
+static hipError_t launch_cfg(int cfg, int wk, bool tapv, const ConvGemmArgs& a,
                              hipStream_t s)
 {
-    if (gemm_cfg_info(cfg).skinny && generic)
+    if (gemm_cfg_info(cfg).skinny && tapv)
         return hipErrorInvalidValue;
     switch (cfg) {
-    case GEMM_128x128:  return launch_lds<T, 128, 128, 2, 2, 8, 2>(generic, a, s);
-    case GEMM_64x64:    return launch_lds<T, 64, 64, 2, 2, 8, 2>(generic, a, s);
-    case GEMM_64x128:   return launch_lds<T, 64, 128, 2, 2, 8, 2>(generic, a, s);
+    case GEMM_128x128:  return launch_lds<T, 128, 128, 2, 2, 8, 2>(tapv, a, s);
+    case GEMM_64x64:    return launch_lds<T, 64, 64, 2, 2, 8, 2>(tapv, a, s);
+    case GEMM_64x128:   return launch_lds<T, 64, 128, 2, 2, 8, 2>(tapv, a, s);
     case GEMM_SK_32x32: return launch_skinny<T, 2, 2>(wk, a, s);
     case GEMM_SK_32x16: return launch_skinny<T, 2, 1>(wk, a, s);
     case GEMM_SK_16x32: return launch_skinny<T, 1, 2>(wk, a, s);
@@ -679,13 +659,13 @@ static hipError_t launch_cfg(int cfg, int wk, bool generic, const ConvGemmArgs& 
     }
 }
 
-hipError_t launch_conv_gemm(int dt, int cfg, int wk, bool generic, const ConvGemmArgs& a,
+hipError_t launch_conv_gemm(int dt, int cfg, int wk, bool tapv, const ConvGemmArgs& a,
                             hipStream_t s)
 {
     switch (dt) {
-    case DT_F32:  return launch_cfg<float>(cfg, wk, generic, a, s);
-    case DT_F16:  return launch_cfg<_Float16>(cfg, wk, generic, a, s);
-    case DT_BF16: return launch_cfg<__bf16>(cfg, wk, generic, a, s);
+    case DT_F32:  return launch_cfg<float>(cfg, wk, tapv, a, s);
+    case DT_F16:  return launch_cfg<_Float16>(cfg, wk, tapv, a, s);
+    case DT_BF16: return launch_cfg<__bf16>(cfg, wk, tapv, a, s);
     default:      return hipErrorInvalidValue;
     }
 }
@@ -730,18 +710,18 @@ static const char* dt_name(int dt)
     return dt == DT_F32 ? "f32" : dt == DT_F16 ? "f16" : "bf16";
 }
 
-const char* conv_gemm_name(int dt, int cfg, int wk, bool generic)
+const char* conv_gemm_name(int dt, int cfg, int wk, bool tapv)
 {
     static char names[3][GEMM_NCFG][SKINNY_MAX_WAVES + 1][2][64];
     const GemmCfgInfo c = gemm_cfg_info(cfg);
     const int w = c.skinny ? wk : 0;
-    char* n = names[dt][cfg][w][generic ? 1 : 0];
+    char* n = names[dt][cfg][w][tapv ? 1 : 0];
     if (!n[0]) {
         if (c.skinny)
             snprintf(n, 64, "conv_gemm_skinny<%s,%dx%d,waves%d>", dt_name(dt), c.bm, c.bn, wk);
         else
             snprintf(n, 64, "conv_gemm<%s,%dx%d,kv%d%s>", dt_name(dt), c.bm, c.bn, c.kv,
-                     generic ? ",gather" : "");
+                     tapv ? ",tapv" : "");
     }
     return n;
 }

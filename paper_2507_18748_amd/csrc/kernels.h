@@ -68,15 +68,24 @@ inline int gemm_bk(int cfg, int dt)
     return (c.skinny ? 4 : c.kv) * (16 / dtype_size(dt));
 }
 
-// Largest K (elements) the generic (scalar-gather) path supports.
-constexpr int GEMM_KTAB_MAX = 2048;
+// Largest number of 16-byte K vectors the per-vector-tap (TAPV) path supports.
+constexpr int GEMM_VTAB_MAX = 1024;
 constexpr int SOFTMAX_MAX_O = 8192;
 constexpr int SKINNY_MAX_WAVES = 16;
 
 // wk: waves per block of the skinny kernel (K split), ignored by the LDS kernel.
-hipError_t launch_conv_gemm(int dt, int cfg, int wk, bool generic, const ConvGemmArgs& a,
+// tapv: the LDS kernel looks up each 16-byte K vector's (kh, kw, ci) in a
+// table (channel count a multiple of the vector width but not of the stage).
+hipError_t launch_conv_gemm(int dt, int cfg, int wk, bool tapv, const ConvGemmArgs& a,
                             hipStream_t s);
-const char* conv_gemm_name(int dt, int cfg, int wk, bool generic);
+const char* conv_gemm_name(int dt, int cfg, int wk, bool tapv);
+
+// Copy NHWC [npix][C] into [npix][Cp] (Cp > C) with zero channels appended,
+// so that a layer with fewer channels than a 16-byte vector can be gathered
+// with vector loads.
+hipError_t launch_pad_channels(int dt, const void* x, void* y, size_t npix, int C, int Cp,
+                               hipStream_t s);
+const char* pad_channels_name(int dt);
 
 // Sum of the split-K partials in split order, then the layer epilogue
 // (scale, bias, residual, activation, rounding; or fp32 logits in softmax mode).

@@ -177,6 +177,26 @@ gap_kernel(const T* __restrict__ x, T* __restrict__ y, int N, int HW, int C)
     }
 }
 
+// One thread per pixel: C channels in, Cp out (zero tail); a 16-byte store
+// when the padded pixel is exactly one vector.
+template <typename T>
+__global__ void __launch_bounds__(256)
+pad_channels_kernel(const T* __restrict__ x, T* __restrict__ y, size_t npix, int C, int Cp)
+{
+    const size_t p = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (p >= npix)
+        return;
+    const T* xp = x + p * C;
+    if (Cp == Vec16<T>::N) {
+        float v[Vec16<T>::N];
+#pragma unroll
+        for (int c = 0; c < Vec16<T>::N; ++c) v[c] = c < C ? (float)xp[c] : 0.0f;
+        Vec16<T>::store(y + p * Cp, v);
+    } else {
+        for (int c = 0; c < Cp; ++c) y[p * Cp + c] = c < C ? xp[c] : (T)0.0f;
+    }
+}
+
 template <typename T>
 __global__ void __launch_bounds__(256) fill_uniform_kernel(T* p, size_t n, uint32_t seed)
 {
@@ -228,6 +248,20 @@ hipError_t launch_gap(int dt, const void* x, void* y, int N, int HW, int C, hipS
     PPIPE_DISPATCH(dt, hipLaunchKernelGGL(gap_kernel<T>, dim3(blocks), dim3(256), 0, s,
                                           (const T*)x, (T*)y, N, HW, C));
     return hipGetLastError();
+}
+
+hipError_t launch_pad_channels(int dt, const void* x, void* y, size_t npix, int C, int Cp,
+                               hipStream_t s)
+{
+    PPIPE_DISPATCH(dt, hipLaunchKernelGGL(pad_channels_kernel<T>, dim3(blocks_for(npix)),
+                                          dim3(256), 0, s, (const T*)x, (T*)y, npix, C, Cp));
+    return hipGetLastError();
+}
+
+const char* pad_channels_name(int dt)
+{
+    static const char* n[3] = {"pad_channels<f32>", "pad_channels<f16>", "pad_channels<bf16>"};
+    return n[dt];
 }
 
 hipError_t launch_fill_uniform(int dt, void* p, size_t n, uint32_t seed, hipStream_t s)

@@ -101,8 +101,9 @@ struct LayerRT {
     int index, op, src, res_src, act, k, stride, pad, groups;
     int H, W, C, Ho, Wo, Co;
     int kind;
-    bool generic = false, softmax = false, skinny_ok = false;
+    bool tapv = false, softmax = false, skinny_ok = false, pad_in = false;
     int KH = 1, KW = 1, gstride = 1, gpad = 0, K = 0, Kpad = 0;
+    int cpad = 0;               // channels as the GEMM reads them (C rounded up to a vector)
     size_t w_off = 0, scale_off = 0, bias_off = 0;
     void* w = nullptr;
     float* scale = nullptr;
@@ -130,6 +131,8 @@ struct ppipe_partition {
     std::vector<size_t> slot_bytes;
     float* ws = nullptr;          // split-K partials, then fp32 logits of a final FC + softmax
     size_t ws_bytes = 0;
+    void* pad_buf = nullptr;      // channel-padded input of layers with C < 16 bytes
+    size_t pad_bytes = 0;
     void* wblob = nullptr;
     size_t wbytes = 0;
     std::vector<uint8_t> host_blob;   // packed parameters between validation and upload
@@ -191,11 +194,11 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok)
     return p;
 }
 
-// The scalar-gather variant applies to the LDS-staged kernel only; a layer
-// planned on the skinny kernel is always vector-loadable (skinny_ok).
-bool gather(const LayerRT& l, const Plan& p)
+// The per-vector-tap variant applies to the LDS-staged kernel only; a layer
+// planned on the skinny kernel has whole K steps per tap (skinny_ok).
+bool tapv_of(const LayerRT& l, const Plan& p)
 {
-    return l.generic && !gemm_cfg_info(p.cfg).skinny;
+    return l.tapv && !gemm_cfg_info(p.cfg).skinny;
 }
 
 const void* buf_ptr(const ppipe_partition* P, int id, const void* in, void* out)
@@ -213,20 +216,33 @@ struct LaunchHook {
     virtual void after(const LayerRT&, int, hipStream_t) {}
 };
 
-int layer_launches(const LayerRT& l, int batch)
+// Launch sequence of a GEMM layer: [channel pad], GEMM, [split-K reduce], [softmax].
+enum LaunchRole { L_PAD, L_GEMM, L_REDUCE, L_SOFTMAX, L_OTHER };
+
+std::vector<int> launch_roles(const LayerRT& l, int batch)
 {
-    if (l.kind != K_GEMM) return 1;
-    return 1 + (l.plans[batch - 1].splits > 1 ? 1 : 0) + (l.softmax ? 1 : 0);
+    if (l.kind != K_GEMM) return {L_OTHER};
+    std::vector<int> r;
+    if (l.pad_in) r.push_back(L_PAD);
+    r.push_back(L_GEMM);
+    if (l.plans[batch - 1].splits > 1) r.push_back(L_REDUCE);
+    if (l.softmax) r.push_back(L_SOFTMAX);
+    return r;
 }
+
+int layer_launches(const LayerRT& l, int batch) { return (int)launch_roles(l, batch).size(); }
 
 std::string launch_name(const ppipe_partition* P, const LayerRT& l, int batch, int launch)
 {
     switch (l.kind) {
     case K_GEMM: {
         const Plan& p = l.plans[batch - 1];
-        if (launch == 0) return conv_gemm_name(P->dtype, p.cfg, p.wk, gather(l, p));
-        if (launch == 1 && p.splits > 1) return splitk_reduce_name(P->dtype);
-        return softmax_rows_name();
+        switch (launch_roles(l, batch)[launch]) {
+        case L_PAD: return pad_channels_name(P->dtype);
+        case L_GEMM: return conv_gemm_name(P->dtype, p.cfg, p.wk, tapv_of(l, p));
+        case L_REDUCE: return splitk_reduce_name(P->dtype);
+        default: return softmax_rows_name();
+        }
     }
     case K_DW: return dwconv_name(P->dtype, l.k);
     case K_MAXPOOL: return maxpool_name(P->dtype);
@@ -235,25 +251,24 @@ std::string launch_name(const ppipe_partition* P, const LayerRT& l, int batch, i
 }
 
 // Algorithmic work of one launch: FLOPs, and the layer's input, weight,
-// output and residual bytes each counted once.  When a layer takes several
-// launches the GEMM owns the FLOPs, input and weights, the last launch the
-// output (and residual); a split-K reduction between them owns nothing.
+// output and residual bytes each counted once.  In a multi-launch layer the
+// first launch owns the input (the GEMM also the weights and FLOPs) and the
+// last launch the output and residual; a split-K reduction in between owns
+// nothing.
 void launch_work(const ppipe_partition* P, const LayerRT& l, int batch, int launch,
                  double* flops, double* bytes)
 {
     const double b = batch;
     const double out_bytes = b * (double)l.out_bytes_b1 *
                              (l.softmax ? 4.0 / dtype_size(P->dtype) : 1.0);
-    const int n = layer_launches(l, batch);
-    const double in_w = b * l.in_bytes_b1 + l.param_bytes;
-    const double out_r = out_bytes + b * l.res_bytes_b1;
-    if (n == 1) {
-        *flops = b * l.flops_b1;
-        *bytes = in_w + out_r;
-        return;
-    }
-    *flops = launch == 0 ? b * l.flops_b1 : 0.0;
-    *bytes = launch == 0 ? in_w : (launch == n - 1 ? out_r : 0.0);
+    const std::vector<int> roles = launch_roles(l, batch);
+    const int n = (int)roles.size(), role = roles[launch];
+    *flops = (role == L_GEMM || role == L_OTHER) ? b * l.flops_b1 : 0.0;
+    double by = 0.0;
+    if (launch == 0) by += b * l.in_bytes_b1;
+    if (role == L_GEMM || role == L_OTHER) by += l.param_bytes;
+    if (launch == n - 1) by += out_bytes + b * l.res_bytes_b1;
+    *bytes = by;
 }
 
 // Enqueue the launches of one layer; only >= 0 restricts to that launch.
@@ -267,8 +282,21 @@ hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, 
     switch (l.kind) {
     case K_GEMM: {
         const Plan& p = l.plans[batch - 1];
+        const std::vector<int> roles = launch_roles(l, batch);
+        auto want = [&](int i) { return only < 0 || only == i; };
+        int li = 0;
+        if (l.pad_in) {
+            if (want(li)) {
+                if (hook) hook->before(l, li, s);
+                e = launch_pad_channels(P->dtype, x, P->pad_buf, (size_t)batch * l.H * l.W, l.C,
+                                        l.cpad, s);
+                if (hook) hook->after(l, li, s);
+                if (e != hipSuccess) return e;
+            }
+            ++li;
+        }
         ConvGemmArgs a;
-        a.x = x;
+        a.x = l.pad_in ? (const void*)P->pad_buf : x;
         a.w = l.w;
         a.scale = l.scale;
         a.bias = l.bias;
@@ -278,7 +306,7 @@ hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, 
         a.partial = P->ws;
         a.logits = P->ws + (p.splits > 1 ? (size_t)p.splits * a.M * l.Co : 0);
         a.N = batch;
-        a.H = l.H; a.W = l.W; a.C = l.C;
+        a.H = l.H; a.W = l.W; a.C = l.cpad;
         a.Ho = l.Ho; a.Wo = l.Wo; a.Co = l.Co;
         a.KH = l.KH; a.KW = l.KW; a.stride = l.gstride; a.pad = l.gpad;
         a.K = l.K; a.Kpad = l.Kpad;
@@ -290,25 +318,28 @@ hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, 
         a.tiles_co = p.tiles_co;
         a.co_fastest = p.co_fastest;
         a.softmax = l.softmax ? 1 : 0;
-        if (only <= 0) {
-            if (hook) hook->before(l, 0, s);
-            e = launch_conv_gemm(P->dtype, p.cfg, p.wk, gather(l, p), a, s);
-            if (hook) hook->after(l, 0, s);
+        if (want(li)) {
+            if (hook) hook->before(l, li, s);
+            e = launch_conv_gemm(P->dtype, p.cfg, p.wk, tapv_of(l, p), a, s);
+            if (hook) hook->after(l, li, s);
+            if (e != hipSuccess) return e;
         }
-        int next = 1;
-        if (e == hipSuccess && p.splits > 1) {
-            if (only < 0 || only == next) {
-                if (hook) hook->before(l, next, s);
+        ++li;
+        if (p.splits > 1) {
+            if (want(li)) {
+                if (hook) hook->before(l, li, s);
                 e = launch_splitk_reduce(P->dtype, a, s);
-                if (hook) hook->after(l, next, s);
+                if (hook) hook->after(l, li, s);
+                if (e != hipSuccess) return e;
             }
-            ++next;
+            ++li;
         }
-        if (e == hipSuccess && l.softmax && (only < 0 || only == next)) {
-            if (hook) hook->before(l, next, s);
+        if (l.softmax && want(li)) {
+            if (hook) hook->before(l, li, s);
             e = launch_softmax_rows(a.logits, a.M, l.Co, (float*)y, s);
-            if (hook) hook->after(l, next, s);
+            if (hook) hook->after(l, li, s);
         }
+        (void)roles;
         return e;
     }
     case K_DW:
@@ -375,6 +406,8 @@ void release(ppipe_partition* P)
     for (void* s : P->slots) (void)hipFree(s);
     P->slots.clear();
     if (P->ws) (void)hipFree(P->ws);
+    if (P->pad_buf) (void)hipFree(P->pad_buf);
+    P->pad_buf = nullptr;
 
     if (P->wblob) (void)hipFree(P->wblob);
     if (P->cap_stream) (void)hipStreamDestroy(P->cap_stream);
@@ -513,27 +546,31 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
             }
             if (o.c % 4)
                 return fail(PPIPE_E_UNSUPPORTED, who + ": output channels must be a multiple of 4");
-            l.K = l.KH * l.KW * x.c;
+            // channels as the GEMM reads them: whole 16-byte vectors
+            l.cpad = (x.c + epv - 1) / epv * epv;
+            l.pad_in = l.cpad != x.c;
+            l.K = l.KH * l.KW * l.cpad;
             l.Kpad = (l.K + 63) / 64 * 64;
-            const int bk_min = gemm_bk(GEMM_128x128, dt);   // every config uses the same BK
-            l.generic = !(x.c % epv == 0 && (l.KH * l.KW == 1 || x.c % bk_min == 0));
+            const int bk = gemm_bk(GEMM_64x64, dt);   // every LDS config uses the same BK
+            // stage-uniform tap (1x1, or C a multiple of the stage) or per-vector taps
+            l.tapv = !(l.KH * l.KW == 1 || l.cpad % bk == 0);
             // skinny kernel: each 64-byte K step lies in one (kh, kw) tap
-            l.skinny_ok = x.c % epv == 0 && (l.KH * l.KW == 1 || x.c % (4 * epv) == 0);
-            if (l.generic && l.Kpad > GEMM_KTAB_MAX)
+            l.skinny_ok = l.KH * l.KW == 1 || l.cpad % (4 * epv) == 0;
+            if (l.tapv && l.Kpad / epv > GEMM_VTAB_MAX)
                 return fail(PPIPE_E_UNSUPPORTED, who + ": reduction length " +
                                                      std::to_string(l.K) + " with C = " +
                                                      std::to_string(x.c) + " is not supported");
             if (!ld.weight)
                 return fail(PPIPE_E_INVALID, who + ": missing weight");
             // operands are addressed with 32-bit byte offsets (buffer loads)
-            if ((double)P->max_batch * x.c * x.h * x.w * esz >= 2147483648.0 ||
+            if ((double)P->max_batch * l.cpad * x.h * x.w * esz >= 2147483648.0 ||
                 (double)o.c * ((l.K + 63) / 64 * 64) * esz >= 2147483648.0)
                 return fail(PPIPE_E_UNSUPPORTED, who + ": input or weights reach 2 GiB at "
                                                        "max_batch");
             if (l.KH > 32 || l.KW > 32)
                 return fail(PPIPE_E_UNSUPPORTED, who + ": window larger than 32");
-            l.flops_b1 = 2.0 * o.c * o.h * o.w * (double)l.K;
-            l.param_bytes = (double)o.c * l.K * esz + 8.0 * o.c;
+            l.flops_b1 = 2.0 * o.c * o.h * o.w * (double)(l.KH * l.KW * x.c);
+            l.param_bytes = (double)o.c * l.KH * l.KW * x.c * esz + 8.0 * o.c;
         } else if (ld.op == PPIPE_OP_MAXPOOL) {
             if (x.c % epv)
                 return fail(PPIPE_E_UNSUPPORTED, who + ": maxpool needs C % " +
@@ -572,23 +609,24 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
         const ppipe_layer_desc& ld = d->layers[l.index];
         if (l.kind == K_GEMM) {
             if (l.op == PPIPE_OP_CONV) {
-                // OIHW [co][ci][kh][kw] -> [co][(kh * KW + kw) * C + ci]
+                // OIHW [co][ci][kh][kw] -> [co][(kh * KW + kw) * cpad + ci]
                 for (int co = 0; co < l.Co; ++co)
                     for (int ci = 0; ci < l.C; ++ci)
                         for (int kh = 0; kh < l.KH; ++kh)
                             for (int kw = 0; kw < l.KW; ++kw)
                                 put_elem(blob, l.w_off, dt,
-                                         (size_t)co * l.Kpad + (size_t)(kh * l.KW + kw) * l.C + ci,
+                                         (size_t)co * l.Kpad + (size_t)(kh * l.KW + kw) * l.cpad + ci,
                                          ld.weight[(((size_t)co * l.C + ci) * l.KH + kh) * l.KW + kw]);
             } else {
-                // [o][c * H * W + h * W + w] -> [o][(h * W + w) * C + c]
+                // [o][c * H * W + h * W + w] -> [o][(h * W + w) * cpad + c]
+                const size_t in_feat = (size_t)l.C * l.KH * l.KW;
                 for (int co = 0; co < l.Co; ++co)
                     for (int c = 0; c < l.C; ++c)
                         for (int h = 0; h < l.KH; ++h)
                             for (int w = 0; w < l.KW; ++w)
                                 put_elem(blob, l.w_off, dt,
-                                         (size_t)co * l.Kpad + (size_t)(h * l.KW + w) * l.C + c,
-                                         ld.weight[(size_t)co * l.K + ((size_t)c * l.KH + h) * l.KW + w]);
+                                         (size_t)co * l.Kpad + (size_t)(h * l.KW + w) * l.cpad + c,
+                                         ld.weight[(size_t)co * in_feat + ((size_t)c * l.KH + h) * l.KW + w]);
             }
         } else {
             // depthwise OIHW [c][1][kh][kw] -> [kh][kw][c]
@@ -669,6 +707,9 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
         }
     }
     P->ws_bytes = ws;
+    for (const LayerRT& l : P->L)
+        if (l.kind == K_GEMM && l.pad_in)
+            P->pad_bytes = std::max(P->pad_bytes, (size_t)P->max_batch * l.H * l.W * l.cpad * esz);
     const LayerRT& last = P->L.back();
     P->in = shape_of(d->layers[begin].src);
     P->out = {last.Co, last.Ho, last.Wo};
@@ -703,6 +744,10 @@ int allocate(ppipe_partition* P)
         if (e != hipSuccess) return fail(PPIPE_E_NOMEM, hip_msg("hipMalloc(split-K)", e));
     }
 
+    if (P->pad_bytes) {
+        e = hipMalloc(&P->pad_buf, P->pad_bytes);
+        if (e != hipSuccess) return fail(PPIPE_E_NOMEM, hip_msg("hipMalloc(channel pad)", e));
+    }
     e = hipStreamCreateWithFlags(&P->cap_stream, hipStreamNonBlocking);
     if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipStreamCreate", e));
     return PPIPE_OK;
@@ -990,7 +1035,7 @@ int ppipe_partition_info(const ppipe_partition* h, ppipe_partition_info_t* info)
     info->in_bytes_per_image = (int64_t)h->in.c * h->in.h * h->in.w * dtype_size(h->dtype);
     info->out_bytes_per_image = (int64_t)h->out.c * h->out.h * h->out.w * dtype_size(h->out_dtype);
     info->weight_bytes = (int64_t)h->wbytes;
-    size_t ws = h->ws_bytes;
+    size_t ws = h->ws_bytes + h->pad_bytes;
     for (size_t b : h->slot_bytes) ws += b;
     info->workspace_bytes = (int64_t)ws;
     return PPIPE_OK;
