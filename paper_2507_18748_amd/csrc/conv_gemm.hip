@@ -600,6 +600,8 @@ GemmCfgInfo gemm_cfg_info(int cfg)
     case GEMM_SK_32x16: return {32, 16, 4, true};
     case GEMM_SK_16x32: return {16, 32, 4, true};
     case GEMM_SK_16x16: return {16, 16, 4, true};
+    case GEMM_128x128_8W: return {128, 128, 8, false};
+    case GEMM_128x64:   return {128, 64, 8, false};
     default:            return {0, 0, 0, false};
     }
 }
@@ -655,6 +657,8 @@ static hipError_t launch_cfg(int cfg, int wk, bool tapv, const ConvGemmArgs& a,
     case GEMM_SK_32x16: return launch_skinny<T, 2, 1>(wk, a, s);
     case GEMM_SK_16x32: return launch_skinny<T, 1, 2>(wk, a, s);
     case GEMM_SK_16x16: return launch_skinny<T, 1, 1>(wk, a, s);
+    case GEMM_128x128_8W: return launch_lds<T, 128, 128, 2, 4, 8, 2>(tapv, a, s);
+    case GEMM_128x64:   return launch_lds<T, 128, 64, 2, 2, 8, 2>(tapv, a, s);
     default:            return hipErrorInvalidValue;
     }
 }
@@ -720,8 +724,8 @@ const char* conv_gemm_name(int dt, int cfg, int wk, bool tapv)
         if (c.skinny)
             snprintf(n, 64, "conv_gemm_skinny<%s,%dx%d,waves%d>", dt_name(dt), c.bm, c.bn, wk);
         else
-            snprintf(n, 64, "conv_gemm<%s,%dx%d,kv%d%s>", dt_name(dt), c.bm, c.bn, c.kv,
-                     tapv ? ",tapv" : "");
+            snprintf(n, 64, "conv_gemm<%s,%dx%d,kv%d%s%s>", dt_name(dt), c.bm, c.bn, c.kv,
+                     cfg == GEMM_128x128_8W ? ",8w" : "", tapv ? ",tapv" : "");
     }
     return n;
 }

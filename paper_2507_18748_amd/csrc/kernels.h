@@ -54,7 +54,9 @@ enum GemmCfg : int {
     GEMM_SK_32x16 = 4,  // skinny 32 co x 16 m
     GEMM_SK_16x32 = 5,  // skinny 16 co x 32 m
     GEMM_SK_16x16 = 6,  // skinny 16x16 tile
-    GEMM_NCFG = 7
+    GEMM_128x128_8W = 7,  // LDS, 8 waves, 64x32 per wave
+    GEMM_128x64 = 8,    // LDS, 4 waves, 64x32 per wave
+    GEMM_NCFG = 9
 };
 struct GemmCfgInfo {
     int bm, bn, kv;       // tile rows (co), columns (m); kv: 16-byte vectors of K per LDS stage

@@ -153,15 +153,33 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok)
         return (int64_t)((M + c.bn - 1) / c.bn) * ((Co + c.bm - 1) / c.bm);
     };
     auto steps = [&](int cfg) { return (K + gemm_bk(cfg, dt) - 1) / gemm_bk(cfg, dt); };
-    int cfg = Co <= 64 && tiles(GEMM_64x128) >= 512 ? GEMM_64x128 : GEMM_64x64, wk = 0;
-    // Few tiles: split K until about two blocks per CU, keeping >= 2 stages
-    // per split (measured on MI355X: the per-block K loop is latency-bound, so
-    // short splits win even after the extra reduction pass).
-    int splits = 1;
-    {
+    // Measured on MI355X over the layers of the five partition workloads:
+    // 8-wave 128x128 tiles win once there are enough of them to fill the chip
+    // (or, with a long K loop, a hundred of them split over K); 64x64 tiles win
+    // everywhere else.  Splitting K pays for the extra reduction pass only when
+    // each split keeps several K steps, and only while the grid is short of
+    // about two blocks per CU.
+    const bool wide = dt != PPIPE_F32 && Co >= 128;
+    const int64_t t128 = tiles(GEMM_128x128_8W);
+    const int k128 = steps(GEMM_128x128_8W);
+    int cfg = GEMM_64x64, wk = 0, splits = 1;
+    if (wide && (t128 >= 384 || (t128 >= 96 && k128 >= 64))) {
+        cfg = GEMM_128x128_8W;
+        if (t128 < 384)
+            while (splits < 16 && t128 * splits * 2 <= 512 && k128 / (splits * 2) >= 8)
+                splits *= 2;
+    } else {
         const int64_t t = tiles(cfg);
-        while (t * splits * 2 <= 512 && steps(cfg) / (splits * 2) >= 2 && splits < 32)
+        const int k = steps(cfg);
+        while (splits < 32) {
+            const int64_t nb = t * splits * 2;
+            const int cps = k / (splits * 2);
+            const bool ok = splits == 1 ? (cps >= 4 && (nb <= 384 || (nb <= 512 && cps >= 8)))
+                                        : ((nb <= 128 && cps >= 2) || (nb <= 384 && cps >= 4) ||
+                                           (nb <= 512 && cps >= 8));
+            if (!ok) break;
             splits *= 2;
+        }
     }
     // PPIPE_GEMM_PLAN="cfg,waves,splits" forces one configuration on every
     // eligible GEMM layer (tuning sweeps and kernel tests).

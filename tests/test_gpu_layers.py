@@ -187,6 +187,8 @@ FORCED = [  # (configuration id, waves, splits): every kernel variant the planne
     ("5,4", "conv_gemm_skinny<", "16x32"), ("5,8", "conv_gemm_skinny<", "16x32"),
     ("6,4", "conv_gemm_skinny<", "16x16"), ("6,8", "conv_gemm_skinny<", "16x16"),
     ("6,16", "conv_gemm_skinny<", "16x16"),
+    ("7,0,1", "conv_gemm<", "128x128,kv8,8w"), ("7,0,2", "conv_gemm<", "128x128,kv8,8w"),
+    ("8,0,1", "conv_gemm<", "128x64"), ("8,0,3", "conv_gemm<", "128x64"),
 ]
 FORCED_SHAPES = {  # ragged M and Co, padded 3x3 taps, a 1x1 with a K tail, an FC + softmax
     "3x3": ((64, 13, 13), [conv("c", -1, 64, 100, 3, 1, 1)], 3, "normal"),
