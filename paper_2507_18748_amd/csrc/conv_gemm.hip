@@ -429,6 +429,206 @@ conv_gemm_kernel(ConvGemmArgs a)
     }
 }
 
+// ---- DMA-staged variant -------------------------------------------------
+// Operand tiles go from global memory straight into LDS with buffer loads in
+// LDS mode (no register staging), into a ring of NS stages, so NS - 1 stages
+// are in flight while the MFMAs consume one.  A stage row is 128 bytes of K
+// with no padding; 16-byte vector kv of row r sits at slot kv ^ dma_swz(r).
+// The MFMA fragment reads take vector kv of 16 consecutive rows, which the
+// swizzle spreads over distinct bank groups (for any 8 consecutive rows, and
+// for the two 128-byte halves a 16-row read covers).
+__device__ __forceinline__ int dma_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+// One 16-byte load per lane from a buffer resource into LDS: lane L writes
+// bytes [lds + 16 L, lds + 16 L + 16); lanes whose offset is beyond the
+// resource range write zeros.  Written as inline assembly so that the compiler
+// does not insert a full wait for all LDS loads before every LDS read; the
+// kernel waits on the vector memory counter itself (dma_wait).  M0 carries the
+// LDS address and needs one wait state before the load.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t lds)
+{
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :: "s"(lds), "v"(voff), "s"(r) : "memory");
+}
+// Wait until at most N of this wave's vector memory operations are pending
+// (they complete in issue order).
+template <int N>
+__device__ __forceinline__ void dma_wait()
+{
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
+}
+
+template <typename T, int BM, int BN, int WM, int WN, int NS, bool TAPV>
+__global__ void __launch_bounds__(WM * WN * 64)
+conv_gemm_dma(ConvGemmArgs a)
+{
+    constexpr int NW = WM * WN;
+    constexpr int ESZ = (int)sizeof(T);
+    constexpr int EPV = 16 / ESZ;
+    constexpr int KV = 8;                      // 16-byte vectors of K per row per stage
+    constexpr int BK = KV * EPV;
+    constexpr int ROW = KV * 16;
+    constexpr int STAGE = (BM + BN) * ROW;
+    constexpr int WTM = BM / WM, WTN = BN / WN;
+    constexpr int FM = WTM / 16, FN = WTN / 16;
+    constexpr int PER_A = BM / (8 * NW), PER_B = BN / (8 * NW);   // loads per lane per stage
+    constexpr int PER = PER_A + PER_B;
+    static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "whole 8-row groups per wave");
+    static_assert(NS >= 2 && (NS - 2) * PER < 64, "ring depth");
+    static_assert(FM >= 1 && FN >= 1 && WTM % 16 == 0 && WTN % 16 == 0, "wave tile");
+
+    extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
+    __shared__ int vtab[TAPV ? GEMM_VTAB_MAX : 1];
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)dyn_smem;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave % WM, wn = wave / WM;
+    const int3 tt = tile_of_block(a);
+    const int m0 = tt.x * BN, co0 = tt.y * BM;
+    const int kc_begin = tt.z * a.chunks_per_split;
+    const int kc_end = min(a.total_chunks, kc_begin + a.chunks_per_split);
+    const int nst = kc_end - kc_begin;
+    const auto wsrc = make_rsrc(a.w, (uint32_t)a.Co * a.Kpad * ESZ);
+    const auto xsrc = make_rsrc(a.x, (uint32_t)a.N * a.H * a.W * a.C * ESZ);
+
+    if constexpr (TAPV) {
+        for (int q = tid; q < a.Kpad / EPV && q < GEMM_VTAB_MAX; q += NW * 64) {
+            int e = -1;
+            const int k = q * EPV;
+            if (k < a.K) {
+                const int tap = k / a.C, ci = k - tap * a.C;
+                const int kh = tap / a.KW, kw = tap - kh * a.KW;
+                e = kh | (kw << 8) | (ci << 16);
+            }
+            vtab[q] = e;
+        }
+        __syncthreads();
+    }
+
+    // Load slots: load i of wave w fills rows 8 (i NW + w) .. + 8 of its
+    // operand; lane L covers row + L / 8, slot L % 8.
+    const int lr = lane >> 3, lp = lane & 7;
+    uint32_t a_off[PER_A];
+#pragma unroll
+    for (int i = 0; i < PER_A; ++i) {
+        const int row = 8 * (i * NW + wave) + lr;
+        const int kv = lp ^ dma_swz(row);
+        a_off[i] = co0 + row < a.Co ? (uint32_t)(((co0 + row) * a.Kpad + kv * EPV) * ESZ) : OOB;
+    }
+    PixelRow b_px[PER_B];
+    int b_k[PER_B];
+#pragma unroll
+    for (int i = 0; i < PER_B; ++i) {
+        const int row = 8 * (i * NW + wave) + lr;
+        b_px[i] = pixel_row(a, m0 + row, ESZ);
+        b_k[i] = lp ^ dma_swz(row);
+    }
+
+    TapCursor cur;
+    int lst = kc_begin;       // next stage to load
+    cur.start(kc_begin * BK, a.C, a.KW);
+    // Stages past the end of this block's K range load nothing (offset OOB)
+    // so that every step issues the same number of loads.
+    auto issue = [&](uint32_t slot) {
+        const bool live = lst < kc_end;
+        const uint32_t k0b = (uint32_t)(lst * BK * ESZ);
+#pragma unroll
+        for (int i = 0; i < PER_A; ++i)
+            dma16(wsrc, live ? a_off[i] + k0b : OOB, slot + (i * NW + wave) * 8 * ROW);
+        const uint32_t bslot = slot + BM * ROW;
+        if constexpr (TAPV) {
+#pragma unroll
+            for (int i = 0; i < PER_B; ++i) {
+                const int e = live ? vtab[lst * KV + b_k[i]] : -1;
+                const int kh = e & 0xff, kw = (e >> 8) & 0xff, ci = e >> 16;
+                const bool ok = e >= 0 && ((b_px[i].hmask >> kh) & (b_px[i].wmask >> kw) & 1u);
+                dma16(xsrc, ok ? (uint32_t)(b_px[i].off + ((kh * a.W + kw) * a.C + ci) * ESZ) : OOB,
+                      bslot + (i * NW + wave) * 8 * ROW);
+            }
+        } else {
+            const int tap_off = ((cur.kh * a.W + cur.kw) * a.C + cur.ci) * ESZ;
+            const int cleft = a.C - cur.ci;
+#pragma unroll
+            for (int i = 0; i < PER_B; ++i) {
+                const bool ok = live &&
+                                ((b_px[i].hmask >> cur.kh) & (b_px[i].wmask >> cur.kw) & 1u) &&
+                                b_k[i] * EPV < cleft;
+                dma16(xsrc, ok ? (uint32_t)(b_px[i].off + tap_off + b_k[i] * 16) : OOB,
+                      bslot + (i * NW + wave) * 8 * ROW);
+            }
+        }
+        if (live) {
+            ++lst;
+            cur.advance(BK, a.C, a.KW);
+        }
+    };
+
+    floatx4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+            acc[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+
+    // fragment offsets within a stage for MFMA k-steps 0 and 1 (vector g and g + 4)
+    const int sw = (lane >> 4) ^ dma_swz(lane & 15);
+    int fa[FM], fb[FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) fa[i] = (wm * WTM + i * 16 + (lane & 15)) * ROW + sw * 16;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) fb[j] = (BM + wn * WTN + j * 16 + (lane & 15)) * ROW + sw * 16;
+
+    if (nst > 0) {
+#pragma unroll
+        for (int p = 0; p < NS - 1; ++p)
+            issue(lds0 + p * STAGE);
+        int rd = 0, wr = NS - 1;
+        for (int s = 0; s < nst; ++s) {
+            dma_wait<(NS - 2) * PER>();   // this wave's loads of stage s have landed
+            __syncthreads();              // ... and every wave's; stage s - 1 is consumed
+            issue(lds0 + wr * STAGE);
+            const unsigned char* S = dyn_smem + rd * STAGE;
+#pragma unroll
+            for (int ks = 0; ks < KV / 4; ++ks) {
+                uint4 af[FM], bf[FN];
+#pragma unroll
+                for (int i = 0; i < FM; ++i) af[i] = *(const uint4*)(S + (fa[i] ^ (ks * 64)));
+#pragma unroll
+                for (int j = 0; j < FN; ++j) bf[j] = *(const uint4*)(S + (fb[j] ^ (ks * 64)));
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < FN; ++j)
+                        Mfma<T>::step(af[i], bf[j], acc[i][j]);
+            }
+            rd = rd + 1 == NS ? 0 : rd + 1;
+            wr = wr + 1 == NS ? 0 : wr + 1;
+        }
+        dma_wait<0>();   // the empty tail loads
+    }
+
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+        const int co = co0 + wm * WTM + i * 16 + 4 * (lane >> 4);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+            const int m = m0 + wn * WTN + j * 16 + (lane & 15);
+            if (co >= a.Co || m >= a.M)
+                continue;
+            if (a.splits > 1) {
+                const floatx4 c = acc[i][j];
+                *(float4*)(a.partial + ((size_t)tt.z * a.M + m) * a.Co + co) =
+                    make_float4(c[0], c[1], c[2], c[3]);
+            } else {
+                store_out4<T>(a, co, m, acc[i][j]);
+            }
+        }
+    }
+}
+
 // Split-K reduction: one thread per 4 output channels of one pixel, partials
 // summed in split order (bitwise deterministic), then the layer epilogue.
 template <typename T>
@@ -602,6 +802,10 @@ GemmCfgInfo gemm_cfg_info(int cfg)
     case GEMM_SK_16x16: return {16, 16, 4, true};
     case GEMM_128x128_8W: return {128, 128, 8, false};
     case GEMM_128x64:   return {128, 64, 8, false};
+    case GEMM_DMA_64x64_S2: return {64, 64, 8, false, 2};
+    case GEMM_DMA_64x64_S3: return {64, 64, 8, false, 3};
+    case GEMM_DMA_128x128_8W_S3: return {128, 128, 8, false, 3};
+    case GEMM_DMA_128x128_8W_S2: return {128, 128, 8, false, 2};
     default:            return {0, 0, 0, false};
     }
 }
@@ -618,6 +822,28 @@ static hipError_t launch_lds(bool tapv, const ConvGemmArgs& a, hipStream_t s)
         hipLaunchKernelGGL((conv_gemm_kernel<T, BM, BN, WM, WN, KV, DEPTH, false>), grid, block,
                            0, s, a);
     return hipGetLastError();
+}
+
+template <typename T, int BM, int BN, int WM, int WN, int NS, bool TAPV>
+static hipError_t launch_dma_one(const ConvGemmArgs& a, hipStream_t s)
+{
+    constexpr int bytes = NS * (BM + BN) * 128;
+    static const hipError_t attr = hipFuncSetAttribute(
+        (const void*)conv_gemm_dma<T, BM, BN, WM, WN, NS, TAPV>,
+        hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (attr != hipSuccess)
+        return attr;
+    hipLaunchKernelGGL((conv_gemm_dma<T, BM, BN, WM, WN, NS, TAPV>),
+                       dim3((unsigned)(a.tiles_m * a.tiles_co * a.splits)), dim3(WM * WN * 64),
+                       bytes, s, a);
+    return hipGetLastError();
+}
+
+template <typename T, int BM, int BN, int WM, int WN, int NS>
+static hipError_t launch_dma(bool tapv, const ConvGemmArgs& a, hipStream_t s)
+{
+    return tapv ? launch_dma_one<T, BM, BN, WM, WN, NS, true>(a, s)
+                : launch_dma_one<T, BM, BN, WM, WN, NS, false>(a, s);
 }
 
 template <typename T, int FM, int FN>
@@ -659,6 +885,10 @@ static hipError_t launch_cfg(int cfg, int wk, bool tapv, const ConvGemmArgs& a,
     case GEMM_SK_16x16: return launch_skinny<T, 1, 1>(wk, a, s);
     case GEMM_128x128_8W: return launch_lds<T, 128, 128, 2, 4, 8, 2>(tapv, a, s);
     case GEMM_128x64:   return launch_lds<T, 128, 64, 2, 2, 8, 2>(tapv, a, s);
+    case GEMM_DMA_64x64_S2: return launch_dma<T, 64, 64, 2, 2, 2>(tapv, a, s);
+    case GEMM_DMA_64x64_S3: return launch_dma<T, 64, 64, 2, 2, 3>(tapv, a, s);
+    case GEMM_DMA_128x128_8W_S3: return launch_dma<T, 128, 128, 2, 4, 3>(tapv, a, s);
+    case GEMM_DMA_128x128_8W_S2: return launch_dma<T, 128, 128, 2, 4, 2>(tapv, a, s);
     default:            return hipErrorInvalidValue;
     }
 }
@@ -723,6 +953,9 @@ const char* conv_gemm_name(int dt, int cfg, int wk, bool tapv)
     if (!n[0]) {
         if (c.skinny)
             snprintf(n, 64, "conv_gemm_skinny<%s,%dx%d,waves%d>", dt_name(dt), c.bm, c.bn, wk);
+        else if (c.dma)
+            snprintf(n, 64, "conv_gemm<%s,%dx%d,kv%d%s,dma%d%s>", dt_name(dt), c.bm, c.bn, c.kv,
+                     c.bm == 128 && c.bn == 128 ? ",8w" : "", c.dma, tapv ? ",tapv" : "");
         else
             snprintf(n, 64, "conv_gemm<%s,%dx%d,kv%d%s%s>", dt_name(dt), c.bm, c.bn, c.kv,
                      cfg == GEMM_128x128_8W ? ",8w" : "", tapv ? ",tapv" : "");

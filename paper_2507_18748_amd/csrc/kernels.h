@@ -56,11 +56,17 @@ enum GemmCfg : int {
     GEMM_SK_16x16 = 6,  // skinny 16x16 tile
     GEMM_128x128_8W = 7,  // LDS, 8 waves, 64x32 per wave
     GEMM_128x64 = 8,    // LDS, 4 waves, 64x32 per wave
-    GEMM_NCFG = 9
+    // Operands loaded straight into a ring of LDS stages (no register staging).
+    GEMM_DMA_64x64_S2 = 9,        // 4 waves, 32x32 per wave, 2 stages
+    GEMM_DMA_64x64_S3 = 10,       // 4 waves, 3 stages
+    GEMM_DMA_128x128_8W_S3 = 11,  // 8 waves, 64x32 per wave, 3 stages
+    GEMM_DMA_128x128_8W_S2 = 12,  // 8 waves, 2 stages
+    GEMM_NCFG = 13
 };
 struct GemmCfgInfo {
     int bm, bn, kv;       // tile rows (co), columns (m); kv: 16-byte vectors of K per LDS stage
     bool skinny;
+    int dma = 0;          // LDS stages of the DMA-staged kernel (0: register-staged)
 };
 GemmCfgInfo gemm_cfg_info(int cfg);
 // K elements per pipeline step: an LDS stage, or one 64-byte MFMA k-step (skinny)

@@ -159,12 +159,13 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok)
     // everywhere else.  Splitting K pays for the extra reduction pass only when
     // each split keeps several K steps, and only while the grid is short of
     // about two blocks per CU.
+    // Both families stage operands with LDS-direct loads in two stages.
     const bool wide = dt != PPIPE_F32 && Co >= 128;
-    const int64_t t128 = tiles(GEMM_128x128_8W);
-    const int k128 = steps(GEMM_128x128_8W);
-    int cfg = GEMM_64x64, wk = 0, splits = 1;
+    const int64_t t128 = tiles(GEMM_DMA_128x128_8W_S2);
+    const int k128 = steps(GEMM_DMA_128x128_8W_S2);
+    int cfg = GEMM_DMA_64x64_S2, wk = 0, splits = 1;
     if (wide && (t128 >= 384 || (t128 >= 96 && k128 >= 64))) {
-        cfg = GEMM_128x128_8W;
+        cfg = GEMM_DMA_128x128_8W_S2;
         if (t128 < 384)
             while (splits < 16 && t128 * splits * 2 <= 512 && k128 / (splits * 2) >= 8)
                 splits *= 2;
@@ -1077,7 +1078,12 @@ int ppipe_layer_info(const ppipe_partition* h, int32_t index, int32_t batch,
     info->flops_b1 = l.flops_b1;
     info->act_bytes_b1 = l.in_bytes_b1 + l.res_bytes_b1 + (double)info->out_bytes_b1;
     info->param_bytes = l.param_bytes;
-    std::string k = launch_name(h, l, batch, 0);
+    // name the GEMM launch of a GEMM layer, not its channel-pad prologue
+    const std::vector<int> roles = launch_roles(l, batch);
+    int main_launch = 0;
+    for (size_t i = 0; i < roles.size(); ++i)
+        if (roles[i] == L_GEMM) main_launch = (int)i;
+    std::string k = launch_name(h, l, batch, main_launch);
     if (l.kind == K_GEMM) {
         const Plan& p = l.plans[batch - 1];
         k += " tiles=" + std::to_string(p.tiles_m * p.tiles_co) + " splits=" +

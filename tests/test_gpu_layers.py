@@ -189,12 +189,18 @@ FORCED = [  # (configuration id, waves, splits): every kernel variant the planne
     ("6,16", "conv_gemm_skinny<", "16x16"),
     ("7,0,1", "conv_gemm<", "128x128,kv8,8w"), ("7,0,2", "conv_gemm<", "128x128,kv8,8w"),
     ("8,0,1", "conv_gemm<", "128x64"), ("8,0,3", "conv_gemm<", "128x64"),
+    ("9,0,1", "conv_gemm<", "64x64,kv8,dma2"), ("9,0,3", "conv_gemm<", "64x64,kv8,dma2"),
+    ("10,0,1", "conv_gemm<", "64x64,kv8,dma3"), ("10,0,2", "conv_gemm<", "64x64,kv8,dma3"),
+    ("11,0,1", "conv_gemm<", "128x128,kv8,8w,dma3"), ("11,0,4", "conv_gemm<", "128x128,kv8,8w,dma3"),
+    ("12,0,1", "conv_gemm<", "128x128,kv8,8w,dma2"), ("12,0,2", "conv_gemm<", "128x128,kv8,8w,dma2"),
 ]
 FORCED_SHAPES = {  # ragged M and Co, padded 3x3 taps, a 1x1 with a K tail, an FC + softmax
     "3x3": ((64, 13, 13), [conv("c", -1, 64, 100, 3, 1, 1)], 3, "normal"),
     "1x1": ((24, 9, 9), [conv("c", -1, 24, 36, act="relu6")], 2, "normal"),
     "fc": ((96, 3, 3), [dict(name="fc", op="fc_softmax", src=-1, c_in=96 * 9, c_out=200,
                              bias=True)], 5, "relu_normal"),
+    # 3-channel stem: channels padded to one vector, per-vector taps
+    "stem": ((3, 23, 23), [conv("c", -1, 3, 64, 7, 2, 3)], 2, "image"),
 }
 
 
@@ -206,6 +212,8 @@ def test_forced_gemm_configuration(monkeypatch, plan, family, tile, shape, dtype
     (forced through the planner override)."""
     from paper_2507_18748_amd import Partition
     in_chw, specs, batch, kind = FORCED_SHAPES[shape]
+    if shape == "stem" and family == "conv_gemm_skinny<":
+        pytest.skip("the skinny kernel has no per-vector-tap gather")
     monkeypatch.setenv("PPIPE_GEMM_PLAN", plan)
     m = make(in_chw, specs)
     with Partition(m.layers, W.model_params(m, 0, dtype), in_chw, 0, 1, dtype,
