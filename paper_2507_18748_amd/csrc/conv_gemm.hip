@@ -156,6 +156,85 @@ __device__ __forceinline__ void store_out4(const ConvGemmArgs& a, int co, int m,
     Vec4<T>::store((T*)a.y + o, v);
 }
 
+// Epilogue of VE consecutive output channels co.. of pixel m from fp32 sums v
+// (VE = 4, or 8 for 16-bit types: one 16-byte vector).
+template <typename T, int VE>
+__device__ __forceinline__ void store_outv(const ConvGemmArgs& a, int co, int m, const float* v)
+{
+    static_assert(VE == 4 || (VE == 8 && sizeof(T) == 2), "vector width");
+    float o[VE];
+#pragma unroll
+    for (int q = 0; q < VE; q += 4) {
+        const float4 sc = *(const float4*)(a.scale + co + q);
+        const float4 bi = *(const float4*)(a.bias + co + q);
+        o[q] = v[q] * sc.x + bi.x;
+        o[q + 1] = v[q + 1] * sc.y + bi.y;
+        o[q + 2] = v[q + 2] * sc.z + bi.z;
+        o[q + 3] = v[q + 3] * sc.w + bi.w;
+    }
+    const size_t off = (size_t)m * a.Co + co;
+    if (a.softmax) {
+#pragma unroll
+        for (int q = 0; q < VE; q += 4)
+            *(float4*)(a.logits + off + q) = make_float4(o[q], o[q + 1], o[q + 2], o[q + 3]);
+        return;
+    }
+    if constexpr (VE == 8) {
+        if (a.res) {
+            const uint4 u = *(const uint4*)((const T*)a.res + off);
+            T r[8];
+            __builtin_memcpy(r, &u, 16);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) o[q] += (float)r[q];
+        }
+        T e[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) e[q] = (T)apply_act(o[q], a.act);
+        uint4 u;
+        __builtin_memcpy(&u, e, 16);
+        *(uint4*)((T*)a.y + off) = u;
+    } else {
+        float4 w = make_float4(o[0], o[1], o[2], o[3]);
+        if (a.res) {
+            const float4 r = Vec4<T>::load((const T*)a.res + off);
+            w.x += r.x; w.y += r.y; w.z += r.z; w.w += r.w;
+        }
+        w.x = apply_act(w.x, a.act); w.y = apply_act(w.y, a.act);
+        w.z = apply_act(w.z, a.act); w.w = apply_act(w.w, a.act);
+        Vec4<T>::store((T*)a.y + off, w);
+    }
+}
+
+// Finish `rows` staged pixel rows of a BM-channel tile (fp32, row pitch LROW
+// floats): VE channels per thread, consecutive threads along a row.  With
+// K splits the raw sums go to the split's partial slice.
+template <typename T, int VE, int BM, int LROW, int NT>
+__device__ __forceinline__ void epi_rows(const ConvGemmArgs& a, const float* ep, int rows,
+                                         int m_base, int co0, int split, int tid)
+{
+    constexpr int VPR = BM / VE;
+    for (int v = tid; v < rows * VPR; v += NT) {
+        const int row = v / VPR, c = (v - row * VPR) * VE;
+        const int m = m_base + row, co = co0 + c;
+        if (m >= a.M || co >= a.Co)
+            continue;
+        float x[VE];
+#pragma unroll
+        for (int q = 0; q < VE; q += 4) {
+            const floatx4 t = *(const floatx4*)(ep + row * LROW + c + q);
+            x[q] = t[0]; x[q + 1] = t[1]; x[q + 2] = t[2]; x[q + 3] = t[3];
+        }
+        if (a.splits > 1) {
+#pragma unroll
+            for (int q = 0; q < VE; q += 4)
+                *(float4*)(a.partial + ((size_t)split * a.M + m) * a.Co + co + q) =
+                    make_float4(x[q], x[q + 1], x[q + 2], x[q + 3]);
+        } else {
+            store_outv<T, VE>(a, co, m, x);
+        }
+    }
+}
+
 // Tile index -> (m tile, co tile) after spreading the 1-D grid over the XCDs
 // in contiguous ranges (the hardware deals block b to XCD b % 8).
 __device__ __forceinline__ int3 tile_of_block(const ConvGemmArgs& a)
@@ -434,10 +513,11 @@ conv_gemm_kernel(ConvGemmArgs a)
 // LDS mode (no register staging), into a ring of NS stages, so NS - 1 stages
 // are in flight while the MFMAs consume one.  A stage row is 128 bytes of K
 // with no padding; 16-byte vector kv of row r sits at slot kv ^ dma_swz(r).
-// The MFMA fragment reads take vector kv of 16 consecutive rows, which the
-// swizzle spreads over distinct bank groups (for any 8 consecutive rows, and
-// for the two 128-byte halves a 16-row read covers).
-__device__ __forceinline__ int dma_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+// The MFMA fragment reads take vector kv of 16 consecutive rows; XOR with the
+// row's low three bits makes these 16-byte reads free of LDS bank conflicts
+// on gfx950 (measured with the SQ_LDS_BANK_CONFLICT counter; plain rows
+// conflict on every read).
+__device__ __forceinline__ int dma_swz(int r) { return r & 7; }
 
 // One 16-byte load per lane from a buffer resource into LDS: lane L writes
 // bytes [lds + 16 L, lds + 16 L + 16); lanes whose offset is beyond the
@@ -610,22 +690,35 @@ conv_gemm_dma(ConvGemmArgs a)
         dma_wait<0>();   // the empty tail loads
     }
 
+    // ---- epilogue staged through LDS ----
+    // The accumulators go to a [pixel][channel] fp32 tile in the (now idle)
+    // stage ring, then each thread finishes VE consecutive channels of one
+    // pixel: scale, bias, residual and activation read and write whole
+    // 16-byte vectors along the NHWC rows.  Tiles larger than the ring are
+    // staged in passes of CH pixel rows (whole wave columns).
+    constexpr int LROW = BM + 4;   // floats per staged pixel row (padding spreads banks)
+    constexpr int CH0 = NS * STAGE / (LROW * 4);
+    constexpr int CH = CH0 >= BN ? BN : CH0 / WTN * WTN;
+    static_assert(CH >= WTN, "the ring holds at least one wave column of the tile");
+    float* ep = (float*)dyn_smem;
 #pragma unroll
-    for (int i = 0; i < FM; ++i) {
-        const int co = co0 + wm * WTM + i * 16 + 4 * (lane >> 4);
+    for (int p0 = 0; p0 < BN; p0 += CH) {
+        __syncthreads();
+        const int wc = wn * WTN;
+        if (wc >= p0 && wc < p0 + CH) {
 #pragma unroll
-        for (int j = 0; j < FN; ++j) {
-            const int m = m0 + wn * WTN + j * 16 + (lane & 15);
-            if (co >= a.Co || m >= a.M)
-                continue;
-            if (a.splits > 1) {
-                const floatx4 c = acc[i][j];
-                *(float4*)(a.partial + ((size_t)tt.z * a.M + m) * a.Co + co) =
-                    make_float4(c[0], c[1], c[2], c[3]);
-            } else {
-                store_out4<T>(a, co, m, acc[i][j]);
-            }
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+                    *(floatx4*)(ep + (wc - p0 + j * 16 + (lane & 15)) * LROW + wm * WTM + i * 16 +
+                                4 * (lane >> 4)) = acc[i][j];
         }
+        __syncthreads();
+        const int rows = min(CH, BN - p0);
+        if (a.Co % EPV == 0)
+            epi_rows<T, EPV, BM, LROW, NW * 64>(a, ep, rows, m0 + p0, co0, tt.z, tid);
+        else
+            epi_rows<T, 4, BM, LROW, NW * 64>(a, ep, rows, m0 + p0, co0, tt.z, tid);
     }
 }
 
@@ -804,8 +897,11 @@ GemmCfgInfo gemm_cfg_info(int cfg)
     case GEMM_128x64:   return {128, 64, 8, false};
     case GEMM_DMA_64x64_S2: return {64, 64, 8, false, 2};
     case GEMM_DMA_64x64_S3: return {64, 64, 8, false, 3};
-    case GEMM_DMA_128x128_8W_S3: return {128, 128, 8, false, 3};
-    case GEMM_DMA_128x128_8W_S2: return {128, 128, 8, false, 2};
+    case GEMM_DMA_128x128_8W_S3: return {128, 128, 8, false, 3, 8};
+    case GEMM_DMA_128x128_8W_S2: return {128, 128, 8, false, 2, 8};
+    case GEMM_DMA_128x128_S2: return {128, 128, 8, false, 2, 4};
+    case GEMM_DMA_128x256_8W_S2: return {128, 256, 8, false, 2, 8};
+    case GEMM_DMA_256x128_8W_S2: return {256, 128, 8, false, 2, 8};
     default:            return {0, 0, 0, false};
     }
 }
@@ -889,6 +985,9 @@ static hipError_t launch_cfg(int cfg, int wk, bool tapv, const ConvGemmArgs& a,
     case GEMM_DMA_64x64_S3: return launch_dma<T, 64, 64, 2, 2, 3>(tapv, a, s);
     case GEMM_DMA_128x128_8W_S3: return launch_dma<T, 128, 128, 2, 4, 3>(tapv, a, s);
     case GEMM_DMA_128x128_8W_S2: return launch_dma<T, 128, 128, 2, 4, 2>(tapv, a, s);
+    case GEMM_DMA_128x128_S2: return launch_dma<T, 128, 128, 2, 2, 2>(tapv, a, s);
+    case GEMM_DMA_128x256_8W_S2: return launch_dma<T, 128, 256, 2, 4, 2>(tapv, a, s);
+    case GEMM_DMA_256x128_8W_S2: return launch_dma<T, 256, 128, 4, 2, 2>(tapv, a, s);
     default:            return hipErrorInvalidValue;
     }
 }
@@ -955,7 +1054,7 @@ const char* conv_gemm_name(int dt, int cfg, int wk, bool tapv)
             snprintf(n, 64, "conv_gemm_skinny<%s,%dx%d,waves%d>", dt_name(dt), c.bm, c.bn, wk);
         else if (c.dma)
             snprintf(n, 64, "conv_gemm<%s,%dx%d,kv%d%s,dma%d%s>", dt_name(dt), c.bm, c.bn, c.kv,
-                     c.bm == 128 && c.bn == 128 ? ",8w" : "", c.dma, tapv ? ",tapv" : "");
+                     c.waves == 8 ? ",8w" : "", c.dma, tapv ? ",tapv" : "");
         else
             snprintf(n, 64, "conv_gemm<%s,%dx%d,kv%d%s%s>", dt_name(dt), c.bm, c.bn, c.kv,
                      cfg == GEMM_128x128_8W ? ",8w" : "", tapv ? ",tapv" : "");

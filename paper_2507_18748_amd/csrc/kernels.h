@@ -61,12 +61,16 @@ enum GemmCfg : int {
     GEMM_DMA_64x64_S3 = 10,       // 4 waves, 3 stages
     GEMM_DMA_128x128_8W_S3 = 11,  // 8 waves, 64x32 per wave, 3 stages
     GEMM_DMA_128x128_8W_S2 = 12,  // 8 waves, 2 stages
-    GEMM_NCFG = 13
+    GEMM_DMA_128x128_S2 = 13,     // 4 waves, 64x64 per wave, 2 stages
+    GEMM_DMA_128x256_8W_S2 = 14,  // 8 waves, 64x64 per wave, 2 stages
+    GEMM_DMA_256x128_8W_S2 = 15,  // 8 waves, 64x64 per wave, 2 stages
+    GEMM_NCFG = 16
 };
 struct GemmCfgInfo {
     int bm, bn, kv;       // tile rows (co), columns (m); kv: 16-byte vectors of K per LDS stage
     bool skinny;
     int dma = 0;          // LDS stages of the DMA-staged kernel (0: register-staged)
+    int waves = 4;        // waves per block (LDS kernels)
 };
 GemmCfgInfo gemm_cfg_info(int cfg);
 // K elements per pipeline step: an LDS stage, or one 64-byte MFMA k-step (skinny)
