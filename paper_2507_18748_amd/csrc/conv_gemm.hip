@@ -510,8 +510,10 @@ conv_gemm_kernel(ConvGemmArgs a)
 
 // ---- DMA-staged variant -------------------------------------------------
 // Operand tiles go from global memory straight into LDS with buffer loads in
-// LDS mode (no register staging), into a ring of NS stages, so NS - 1 stages
-// are in flight while the MFMAs consume one.  A stage row is 128 bytes of K
+// LDS mode (no register staging), into a ring of NS stages.  With NS = 2 the
+// next stage loads while the MFMAs consume the current one; with NS >= 3 the
+// loop is software-pipelined (NS - 2 stages in flight, the fragment reads of
+// stage s pending while the MFMAs of stage s - 1 run).  A stage row is 128 bytes of K
 // with no padding; 16-byte vector kv of row r sits at slot kv ^ dma_swz(r).
 // The MFMA fragment reads take vector kv of 16 consecutive rows; XOR with the
 // row's low three bits makes these 16-byte reads free of LDS bank conflicts
@@ -555,7 +557,7 @@ conv_gemm_dma(ConvGemmArgs a)
     constexpr int PER_A = BM / (8 * NW), PER_B = BN / (8 * NW);   // loads per lane per stage
     constexpr int PER = PER_A + PER_B;
     static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "whole 8-row groups per wave");
-    static_assert(NS >= 2 && (NS - 2) * PER < 64, "ring depth");
+    static_assert(NS >= 2 && (NS == 2 || (NS - 3) * PER < 64), "ring depth");
     static_assert(FM >= 1 && FN >= 1 && WTM % 16 == 0 && WTN % 16 == 0, "wave tile");
 
     extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
@@ -661,34 +663,88 @@ conv_gemm_dma(ConvGemmArgs a)
 #pragma unroll
     for (int j = 0; j < FN; ++j) fb[j] = (BM + wn * WTN + j * 16 + (lane & 15)) * ROW + sw * 16;
 
-    if (nst > 0) {
+    // Software pipeline: the MFMAs of stage s - 1 run from registers while the
+    // fragment reads of stage s are in flight, and loads run NS - 2 stages
+    // ahead.  Step s waits for stage s, then refills the slot of stage s - 2
+    // (every wave finished its MFMAs on that stage before the barrier).  Two
+    // named fragment sets, loop unrolled by two, keep register indices constant.
+    uint4 xa0[KV / 4][FM], xb0[KV / 4][FN], xa1[KV / 4][FM], xb1[KV / 4][FN];
+#define PPIPE_READ(S, XA, XB)                                                                     \
+    do {                                                                                          \
+        _Pragma("unroll") for (int ks = 0; ks < KV / 4; ++ks) {                                   \
+            _Pragma("unroll") for (int i = 0; i < FM; ++i)                                        \
+                XA[ks][i] = *(const uint4*)((S) + (fa[i] ^ (ks * 64)));                           \
+            _Pragma("unroll") for (int j = 0; j < FN; ++j)                                        \
+                XB[ks][j] = *(const uint4*)((S) + (fb[j] ^ (ks * 64)));                           \
+        }                                                                                         \
+    } while (0)
+#define PPIPE_MMA(XA, XB)                                                                         \
+    do {                                                                                          \
+        _Pragma("unroll") for (int ks = 0; ks < KV / 4; ++ks)                                     \
+            _Pragma("unroll") for (int i = 0; i < FM; ++i)                                        \
+                _Pragma("unroll") for (int j = 0; j < FN; ++j)                                    \
+                    Mfma<T>::step(XA[ks][i], XB[ks][j], acc[i][j]);                               \
+    } while (0)
+#define PPIPE_DSTEP(s, XA, XB, YA, YB)                                                            \
+    do {                                                                                          \
+        dma_wait<(NS - 3) * PER>();   /* this wave's loads of stage s have landed */              \
+        __syncthreads();              /* ... and every wave's; stage s - 2 is consumed */         \
+        issue(lds0 + wr * STAGE);                                                                 \
+        PPIPE_READ(dyn_smem + rd * STAGE, XA, XB);                                                \
+        if ((s) > 0)                                                                              \
+            PPIPE_MMA(YA, YB);                                                                    \
+        rd = rd + 1 == NS ? 0 : rd + 1;                                                           \
+        wr = wr + 1 == NS ? 0 : wr + 1;                                                           \
+    } while (0)
+    if constexpr (NS == 2) {
+// Two stages: the load of stage s + 1 runs while the MFMAs consume
+        // stage s; fragment reads and MFMAs of a stage run back to back.  The
+        // lowest register pressure and LDS footprint of the variants, for
+        // layers with several blocks per CU.
+        if (nst > 0) {
+            issue(lds0);
+            for (int s = 0; s < nst; ++s) {
+                dma_wait<0>();     // this wave's loads of stage s have landed
+                __syncthreads();   // ... and every wave's; stage s - 1 is consumed
+                issue(lds0 + ((s + 1) & 1) * STAGE);
+                const unsigned char* S = dyn_smem + (s & 1) * STAGE;
 #pragma unroll
-        for (int p = 0; p < NS - 1; ++p)
-            issue(lds0 + p * STAGE);
-        int rd = 0, wr = NS - 1;
-        for (int s = 0; s < nst; ++s) {
-            dma_wait<(NS - 2) * PER>();   // this wave's loads of stage s have landed
-            __syncthreads();              // ... and every wave's; stage s - 1 is consumed
-            issue(lds0 + wr * STAGE);
-            const unsigned char* S = dyn_smem + rd * STAGE;
+                for (int ks = 0; ks < KV / 4; ++ks) {
+                    uint4 af[FM], bf[FN];
 #pragma unroll
-            for (int ks = 0; ks < KV / 4; ++ks) {
-                uint4 af[FM], bf[FN];
+                    for (int i = 0; i < FM; ++i) af[i] = *(const uint4*)(S + (fa[i] ^ (ks * 64)));
 #pragma unroll
-                for (int i = 0; i < FM; ++i) af[i] = *(const uint4*)(S + (fa[i] ^ (ks * 64)));
+                    for (int j = 0; j < FN; ++j) bf[j] = *(const uint4*)(S + (fb[j] ^ (ks * 64)));
 #pragma unroll
-                for (int j = 0; j < FN; ++j) bf[j] = *(const uint4*)(S + (fb[j] ^ (ks * 64)));
+                    for (int i = 0; i < FM; ++i)
 #pragma unroll
-                for (int i = 0; i < FM; ++i)
-#pragma unroll
-                    for (int j = 0; j < FN; ++j)
-                        Mfma<T>::step(af[i], bf[j], acc[i][j]);
+                        for (int j = 0; j < FN; ++j)
+                            Mfma<T>::step(af[i], bf[j], acc[i][j]);
+                }
             }
-            rd = rd + 1 == NS ? 0 : rd + 1;
-            wr = wr + 1 == NS ? 0 : wr + 1;
+            dma_wait<0>();   // the empty tail load
+        }
+    } else if (nst > 0) {
+#pragma unroll
+        for (int p = 0; p < NS - 2; ++p)
+            issue(lds0 + p * STAGE);
+        int rd = 0, wr = NS - 2;   // slot of stage s; slot that receives stage s + NS - 2
+        int s = 0;
+        for (; s + 1 < nst; s += 2) {
+            PPIPE_DSTEP(s, xa0, xb0, xa1, xb1);
+            PPIPE_DSTEP(s + 1, xa1, xb1, xa0, xb0);
+        }
+        if (s < nst) {
+            PPIPE_DSTEP(s, xa0, xb0, xa1, xb1);
+            PPIPE_MMA(xa0, xb0);
+        } else {
+            PPIPE_MMA(xa1, xb1);
         }
         dma_wait<0>();   // the empty tail loads
     }
+#undef PPIPE_DSTEP
+#undef PPIPE_MMA
+#undef PPIPE_READ
 
     // ---- epilogue staged through LDS ----
     // The accumulators go to a [pixel][channel] fp32 tile in the (now idle)
@@ -895,13 +951,10 @@ GemmCfgInfo gemm_cfg_info(int cfg)
     case GEMM_SK_16x16: return {16, 16, 4, true};
     case GEMM_128x128_8W: return {128, 128, 8, false};
     case GEMM_128x64:   return {128, 64, 8, false};
-    case GEMM_DMA_64x64_S2: return {64, 64, 8, false, 2};
-    case GEMM_DMA_64x64_S3: return {64, 64, 8, false, 3};
-    case GEMM_DMA_128x128_8W_S3: return {128, 128, 8, false, 3, 8};
+    case GEMM_DMA_64x64_S2: return {64, 64, 8, false, 2, 4};
+    case GEMM_DMA_64x64_S3: return {64, 64, 8, false, 3, 4};
     case GEMM_DMA_128x128_8W_S2: return {128, 128, 8, false, 2, 8};
-    case GEMM_DMA_128x128_S2: return {128, 128, 8, false, 2, 4};
-    case GEMM_DMA_128x256_8W_S2: return {128, 256, 8, false, 2, 8};
-    case GEMM_DMA_256x128_8W_S2: return {256, 128, 8, false, 2, 8};
+    case GEMM_DMA_128x128_8W_S3: return {128, 128, 8, false, 3, 8};
     default:            return {0, 0, 0, false};
     }
 }
@@ -983,11 +1036,8 @@ static hipError_t launch_cfg(int cfg, int wk, bool tapv, const ConvGemmArgs& a,
     case GEMM_128x64:   return launch_lds<T, 128, 64, 2, 2, 8, 2>(tapv, a, s);
     case GEMM_DMA_64x64_S2: return launch_dma<T, 64, 64, 2, 2, 2>(tapv, a, s);
     case GEMM_DMA_64x64_S3: return launch_dma<T, 64, 64, 2, 2, 3>(tapv, a, s);
-    case GEMM_DMA_128x128_8W_S3: return launch_dma<T, 128, 128, 2, 4, 3>(tapv, a, s);
     case GEMM_DMA_128x128_8W_S2: return launch_dma<T, 128, 128, 2, 4, 2>(tapv, a, s);
-    case GEMM_DMA_128x128_S2: return launch_dma<T, 128, 128, 2, 2, 2>(tapv, a, s);
-    case GEMM_DMA_128x256_8W_S2: return launch_dma<T, 128, 256, 2, 4, 2>(tapv, a, s);
-    case GEMM_DMA_256x128_8W_S2: return launch_dma<T, 256, 128, 4, 2, 2>(tapv, a, s);
+    case GEMM_DMA_128x128_8W_S3: return launch_dma<T, 128, 128, 2, 4, 3>(tapv, a, s);
     default:            return hipErrorInvalidValue;
     }
 }

@@ -58,13 +58,10 @@ enum GemmCfg : int {
     GEMM_128x64 = 8,    // LDS, 4 waves, 64x32 per wave
     // Operands loaded straight into a ring of LDS stages (no register staging).
     GEMM_DMA_64x64_S2 = 9,        // 4 waves, 32x32 per wave, 2 stages
-    GEMM_DMA_64x64_S3 = 10,       // 4 waves, 3 stages
-    GEMM_DMA_128x128_8W_S3 = 11,  // 8 waves, 64x32 per wave, 3 stages
-    GEMM_DMA_128x128_8W_S2 = 12,  // 8 waves, 2 stages
-    GEMM_DMA_128x128_S2 = 13,     // 4 waves, 64x64 per wave, 2 stages
-    GEMM_DMA_128x256_8W_S2 = 14,  // 8 waves, 64x64 per wave, 2 stages
-    GEMM_DMA_256x128_8W_S2 = 15,  // 8 waves, 64x64 per wave, 2 stages
-    GEMM_NCFG = 16
+    GEMM_DMA_64x64_S3 = 10,       // 4 waves, 3 stages, software-pipelined
+    GEMM_DMA_128x128_8W_S2 = 11,  // 8 waves, 64x32 per wave, 2 stages
+    GEMM_DMA_128x128_8W_S3 = 12,  // 8 waves, 3 stages, software-pipelined
+    GEMM_NCFG = 13
 };
 struct GemmCfgInfo {
     int bm, bn, kv;       // tile rows (co), columns (m); kv: 16-byte vectors of K per LDS stage

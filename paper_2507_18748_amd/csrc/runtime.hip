@@ -159,16 +159,21 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok)
     // everywhere else.  Splitting K pays for the extra reduction pass only when
     // each split keeps several K steps, and only while the grid is short of
     // about two blocks per CU.
-    // Both families stage operands with LDS-direct loads in two stages.
+    // Both families stage operands with LDS-direct loads.  Dense grids take
+    // the two-stage loop (lowest registers and LDS, highest occupancy); sparse
+    // grids (under two 64x64 blocks, or one 8-wave block, per CU) take the
+    // software-pipelined loop.
     const bool wide = dt != PPIPE_F32 && Co >= 128;
     const int64_t t128 = tiles(GEMM_DMA_128x128_8W_S2);
     const int k128 = steps(GEMM_DMA_128x128_8W_S2);
     int cfg = GEMM_DMA_64x64_S2, wk = 0, splits = 1;
-    if (wide && (t128 >= 384 || (t128 >= 96 && k128 >= 64))) {
+    if (wide && (t128 >= 192 || (t128 >= 96 && k128 >= 64))) {
         cfg = GEMM_DMA_128x128_8W_S2;
-        if (t128 < 384)
+        if (t128 < 192)
             while (splits < 16 && t128 * splits * 2 <= 512 && k128 / (splits * 2) >= 8)
                 splits *= 2;
+        if (t128 * splits < 256)
+            cfg = GEMM_DMA_128x128_8W_S3;
     } else {
         const int64_t t = tiles(cfg);
         const int k = steps(cfg);
@@ -181,6 +186,8 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok)
             if (!ok) break;
             splits *= 2;
         }
+        if (t * splits < 512)
+            cfg = GEMM_DMA_64x64_S3;
     }
     // PPIPE_GEMM_PLAN="cfg,waves,splits" forces one configuration on every
     // eligible GEMM layer (tuning sweeps and kernel tests).
