@@ -917,25 +917,61 @@ conv_gemm_skinny(ConvGemmArgs a)
     }
 }
 
-// Softmax of each row of fp32 logits; one wave per row.
+// Softmax of each row, one block of 256 threads per row with the row held in
+// registers (VPT values per thread).  With K splits the block first sums the
+// raw partial rows in split order and applies the FC epilogue (scale, bias),
+// so the reduction and the softmax are one launch.
+template <int VPT>
 __global__ void __launch_bounds__(256)
-softmax_rows_kernel(const float* __restrict__ z, int M, int O, float* __restrict__ out)
+softmax_rows_kernel(const float* __restrict__ z, int splits, const float* __restrict__ scale,
+                    const float* __restrict__ bias, int M, int O, float* __restrict__ out)
 {
-    const int lane = threadIdx.x & 63;
-    const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (m >= M)
-        return;
+    __shared__ float red[2][4];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int m = blockIdx.x;
+    const size_t plane = (size_t)M * O;
     const float* zr = z + (size_t)m * O;
+    float v[VPT];
+#pragma unroll
+    for (int q = 0; q < VPT; ++q) {
+        const int o = t + q * 256;
+        v[q] = o < O ? zr[o] : 0.0f;
+    }
+    for (int sp = 1; sp < splits; ++sp)
+#pragma unroll
+        for (int q = 0; q < VPT; ++q) {
+            const int o = t + q * 256;
+            if (o < O) v[q] += zr[sp * plane + o];
+        }
     float mx = -INFINITY;
-    for (int o = lane; o < O; o += 64)
-        mx = fmaxf(mx, zr[o]);
+#pragma unroll
+    for (int q = 0; q < VPT; ++q) {
+        const int o = t + q * 256;
+        if (o < O) {
+            if (scale) v[q] = v[q] * scale[o] + bias[o];
+            mx = fmaxf(mx, v[q]);
+        }
+    }
     mx = wave_max(mx);
+    if (lane == 0) red[0][wave] = mx;
+    __syncthreads();
+    mx = fmaxf(fmaxf(red[0][0], red[0][1]), fmaxf(red[0][2], red[0][3]));
     float sum = 0.0f;
-    for (int o = lane; o < O; o += 64)
-        sum += expf(zr[o] - mx);
-    const float inv = 1.0f / wave_sum(sum);
-    for (int o = lane; o < O; o += 64)
-        out[(size_t)m * O + o] = expf(zr[o] - mx) * inv;
+#pragma unroll
+    for (int q = 0; q < VPT; ++q) {
+        const int o = t + q * 256;
+        v[q] = o < O ? expf(v[q] - mx) : 0.0f;
+        sum += v[q];
+    }
+    sum = wave_sum(sum);
+    if (lane == 0) red[1][wave] = sum;
+    __syncthreads();
+    const float inv = 1.0f / (red[1][0] + red[1][1] + red[1][2] + red[1][3]);
+#pragma unroll
+    for (int q = 0; q < VPT; ++q) {
+        const int o = t + q * 256;
+        if (o < O) out[(size_t)m * O + o] = v[q] * inv;
+    }
 }
 
 // ---- host-side launchers ----
@@ -1053,10 +1089,21 @@ hipError_t launch_conv_gemm(int dt, int cfg, int wk, bool tapv, const ConvGemmAr
     }
 }
 
-hipError_t launch_softmax_rows(const float* logits, int M, int O, float* out, hipStream_t s)
+hipError_t launch_softmax_rows(const float* z, int splits, const float* scale, const float* bias,
+                               int M, int O, float* out, hipStream_t s)
 {
-    hipLaunchKernelGGL(softmax_rows_kernel, dim3((M + 3) / 4), dim3(256), 0, s, logits, M, O,
-                       out);
+    static_assert(SOFTMAX_MAX_O <= 256 * 32, "row fits the register array");
+    if (O <= 1024)
+        hipLaunchKernelGGL(softmax_rows_kernel<4>, dim3(M), dim3(256), 0, s, z, splits, scale,
+                           bias, M, O, out);
+    else if (O <= 2048)
+        hipLaunchKernelGGL(softmax_rows_kernel<8>, dim3(M), dim3(256), 0, s, z, splits, scale,
+                           bias, M, O, out);
+    else if (O <= SOFTMAX_MAX_O)
+        hipLaunchKernelGGL(softmax_rows_kernel<32>, dim3(M), dim3(256), 0, s, z, splits, scale,
+                           bias, M, O, out);
+    else
+        return hipErrorInvalidValue;
     return hipGetLastError();
 }
 

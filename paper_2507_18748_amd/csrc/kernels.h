@@ -101,8 +101,11 @@ const char* pad_channels_name(int dt);
 hipError_t launch_splitk_reduce(int dt, const ConvGemmArgs& a, hipStream_t s);
 const char* splitk_reduce_name(int dt);
 
-// Row-wise softmax of fp32 logits [M][O] into out [M][O].
-hipError_t launch_softmax_rows(const float* logits, int M, int O, float* out, hipStream_t s);
+// Row-wise softmax into out [M][O] of fp32 logits z [M][O] (splits = 1,
+// scale = bias = nullptr), or of raw split-K sums z [splits][M][O] finished
+// as scale[o] * sum + bias[o] (the FC epilogue) before the softmax.
+hipError_t launch_softmax_rows(const float* z, int splits, const float* scale, const float* bias,
+                               int M, int O, float* out, hipStream_t s);
 const char* softmax_rows_name();
 
 // Depthwise k x k convolution (NHWC, weights [k][k][C] in dtype) with the

@@ -251,7 +251,8 @@ std::vector<int> launch_roles(const LayerRT& l, int batch)
     std::vector<int> r;
     if (l.pad_in) r.push_back(L_PAD);
     r.push_back(L_GEMM);
-    if (l.plans[batch - 1].splits > 1) r.push_back(L_REDUCE);
+    // the softmax launch of an FC + softmax layer also reduces its K splits
+    if (l.plans[batch - 1].splits > 1 && !l.softmax) r.push_back(L_REDUCE);
     if (l.softmax) r.push_back(L_SOFTMAX);
     return r;
 }
@@ -351,7 +352,7 @@ hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, 
             if (e != hipSuccess) return e;
         }
         ++li;
-        if (p.splits > 1) {
+        if (p.splits > 1 && !l.softmax) {
             if (want(li)) {
                 if (hook) hook->before(l, li, s);
                 e = launch_splitk_reduce(P->dtype, a, s);
@@ -362,7 +363,10 @@ hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, 
         }
         if (l.softmax && want(li)) {
             if (hook) hook->before(l, li, s);
-            e = launch_softmax_rows(a.logits, a.M, l.Co, (float*)y, s);
+            e = p.splits > 1 ? launch_softmax_rows(a.partial, p.splits, l.scale, l.bias, a.M,
+                                                   l.Co, (float*)y, s)
+                             : launch_softmax_rows(a.logits, 1, nullptr, nullptr, a.M, l.Co,
+                                                   (float*)y, s);
             if (hook) hook->after(l, li, s);
         }
         (void)roles;
