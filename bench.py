@@ -44,12 +44,42 @@ def roofline(records, dtype):
         achieved = g["bytes"] / g["n"] / (avg_us * 1e-6) / 1e9
         out = {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s"}
     out["frac"] = out["achieved"] / out["peak"]
-    out["traffic"] = None
+    out["traffic"] = None   # filled from committed HBM counters, see measured_traffic
     out["kernel"] = name
     out["launches_per_step"] = g["n"]
     out["avg_launch_us"] = avg_us
     out["share_of_step"] = g["us"] / sum(v["us"] for v in groups.values())
     return out
+
+
+def source_digest():
+    """sha256 over the kernel and runtime sources (any change invalidates
+    HBM counters taken before it)."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2507_18748_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` on `workload` from a committed counter
+    record (profiles/*_traffic.json: FETCH_SIZE and WRITE_SIZE per dispatch,
+    scaled by a plain copy's counters), or None when there is none or the
+    sources changed since the counters were taken."""
+    import glob
+    digest = None
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*_traffic.json"))):
+        with open(path) as f:
+            rec = json.load(f)
+        if rec.get("workload") != workload or rec.get("kernel") != kernel:
+            continue
+        digest = digest or source_digest()
+        if rec.get("source_sha256") == digest:
+            return rec["traffic_bytes_per_launch"]
+    return None
 
 
 def cpu_baseline(wl, m, P, target_s):
@@ -143,6 +173,8 @@ def main():
     ap.add_argument("--workload", default="resnet50_layer4_head")
     ap.add_argument("--batch", type=int, default=0, help="override the workload batch")
     ap.add_argument("--no-graph", action="store_true", help="launch kernels directly")
+    ap.add_argument("--timing-steps", type=int, default=20,
+                    help="directly launched steps whose per-launch events give the roofline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="oracle sample length for cpu_baseline (0 disables)")
     ap.add_argument("--profile-reps", type=int, default=50)
@@ -221,8 +253,28 @@ def main():
     print(f"[bench] timed {args.steps} steps: wall {wall * 1e3:.2f} ms, events {gpu_ms:.2f} ms",
           file=sys.stderr, flush=True)
 
-    recs = part.profile_kernels(wl.batch, warmup=10, reps=args.profile_reps)
+    # Launch durations: right after the timed region, steps launched directly
+    # in the same layer order, each launch recording a pair of HIP events
+    # around the kernel itself on the stream the kernels run on (events inside
+    # a replayed graph cannot be timed on ROCm).  Mean over the steps.
+    part.timing_setup(wl.batch, xd.data_ptr(), out.data_ptr())
+    part.run_timed(sp)
+    recs = None
+    for _ in range(args.timing_steps):
+        part.run_timed(sp)
+        r = part.timing_read()
+        if recs is None:
+            recs = r
+        else:
+            for a, b in zip(recs, r):
+                a["mean_us"] += b["mean_us"]
+    for a in recs:
+        a["mean_us"] /= args.timing_steps
+        a["median_us"] = a["min_us"] = a["mean_us"]
     roof = roofline(recs, wl.dtype)
+    roof["traffic"] = measured_traffic(wl.name, roof["kernel"])
+    roof["timing"] = (f"HIP events recorded by each launch, {args.timing_steps} directly "
+                      f"launched steps after the timed region")
     if args.kernels:
         with open(args.kernels, "w") as f:
             json.dump(recs, f, indent=1)

@@ -169,6 +169,26 @@ int ppipe_profile_kernels(ppipe_partition* h, int32_t batch, int32_t warmup,
                           int32_t reps, ppipe_kernel_record* records,
                           int32_t capacity, int32_t* count);
 
+/* Launch timing.  Prepares (batch, in, out) for ppipe_partition_run_timed:
+ * every kernel launch of a timed run records a pair of HIP events around
+ * the kernel itself (hipExtLaunchKernel), on the run's stream, with no
+ * packets between the kernels.  Timed runs launch directly: events recorded
+ * inside a replayed graph cannot be timed on ROCm.  Allocates the events;
+ * replaces an earlier set-up of the handle.  Returns a status. */
+int ppipe_timing_setup(ppipe_partition* h, int32_t batch, const void* in, void* out);
+
+/* One run of the set-up (batch, in, out) on `stream` with its launch events.
+ * Asynchronous; each run overwrites the previous run's event times.
+ * Returns a status (PPIPE_E_INVALID without a set-up). */
+int ppipe_partition_run_timed(ppipe_partition* h, void* stream);
+
+/* Durations of the launches of the most recent timed run, in launch order,
+ * as records like ppipe_profile_kernels' with mean = median = min = that
+ * run's duration.  Waits for the run's last event.  Writes up to `capacity`
+ * records and sets *count to the launches per run.  Returns a status. */
+int ppipe_timing_read(ppipe_partition* h, ppipe_kernel_record* records, int32_t capacity,
+                      int32_t* count);
+
 int ppipe_partition_info(const ppipe_partition* h, ppipe_partition_info_t* info);
 
 /* Static description of global layer `index` (begin <= index < end) with the

@@ -34,6 +34,12 @@ class ModelDesc(ctypes.Structure):
                 ("max_batch", ctypes.c_int32)]
 
 
+def _records(recs, count: int, cap: int) -> List[dict]:
+    return [{"layer": r.layer, "launch": r.launch, "kernel": r.kernel.decode(),
+             "flops": r.flops, "bytes": r.bytes, "mean_us": r.mean_us,
+             "median_us": r.median_us, "min_us": r.min_us} for r in recs[:min(count, cap)]]
+
+
 class PartitionInfo(ctypes.Structure):
     _fields_ = [("layer_begin", ctypes.c_int32), ("layer_end", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("max_batch", ctypes.c_int32),
@@ -99,6 +105,13 @@ def load_library() -> ctypes.CDLL:
     lib.ppipe_profile_kernels.restype = ctypes.c_int
     lib.ppipe_profile_kernels.argtypes = [vp, i32, i32, i32, ctypes.POINTER(KernelRecord), i32,
                                           ctypes.POINTER(i32)]
+    lib.ppipe_timing_setup.restype = ctypes.c_int
+    lib.ppipe_timing_setup.argtypes = [vp, i32, vp, vp]
+    lib.ppipe_partition_run_timed.restype = ctypes.c_int
+    lib.ppipe_partition_run_timed.argtypes = [vp, vp]
+    lib.ppipe_timing_read.restype = ctypes.c_int
+    lib.ppipe_timing_read.argtypes = [vp, ctypes.POINTER(KernelRecord), i32,
+                                      ctypes.POINTER(i32)]
     lib.ppipe_partition_info.restype = ctypes.c_int
     lib.ppipe_partition_info.argtypes = [vp, ctypes.POINTER(PartitionInfo)]
     lib.ppipe_layer_info.restype = ctypes.c_int
@@ -202,12 +215,21 @@ class Partition:
         recs = (KernelRecord * cap)()
         self._check(self._lib.ppipe_profile_kernels(self._h, batch, warmup, reps, recs, cap,
                                                     ctypes.byref(count)))
-        out = []
-        for r in recs[:min(count.value, cap)]:
-            out.append({"layer": r.layer, "launch": r.launch, "kernel": r.kernel.decode(),
-                        "flops": r.flops, "bytes": r.bytes, "mean_us": r.mean_us,
-                        "median_us": r.median_us, "min_us": r.min_us})
-        return out
+        return _records(recs, count.value, cap)
+
+    # --- launch timing inside runs ---
+    def timing_setup(self, batch: int, x_ptr: int, out_ptr: int):
+        self._check(self._lib.ppipe_timing_setup(self._h, batch, x_ptr, out_ptr))
+
+    def run_timed(self, stream: int = 0):
+        self._check(self._lib.ppipe_partition_run_timed(self._h, stream))
+
+    def timing_read(self) -> List[dict]:
+        count = ctypes.c_int32(0)
+        cap = 4 * (self.end - self.begin) + 8
+        recs = (KernelRecord * cap)()
+        self._check(self._lib.ppipe_timing_read(self._h, recs, cap, ctypes.byref(count)))
+        return _records(recs, count.value, cap)
 
     def layer_info(self, index: int, batch: int = 1) -> dict:
         li = LayerInfo()

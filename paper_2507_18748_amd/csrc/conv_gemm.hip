@@ -1001,10 +1001,10 @@ static hipError_t launch_lds(bool tapv, const ConvGemmArgs& a, hipStream_t s)
     dim3 grid((unsigned)(a.tiles_m * a.tiles_co * a.splits));
     dim3 block(WM * WN * 64);
     if (tapv)
-        hipLaunchKernelGGL((conv_gemm_kernel<T, BM, BN, WM, WN, KV, DEPTH, true>), grid, block,
+        PPIPE_LAUNCH((conv_gemm_kernel<T, BM, BN, WM, WN, KV, DEPTH, true>), grid, block,
                            0, s, a);
     else
-        hipLaunchKernelGGL((conv_gemm_kernel<T, BM, BN, WM, WN, KV, DEPTH, false>), grid, block,
+        PPIPE_LAUNCH((conv_gemm_kernel<T, BM, BN, WM, WN, KV, DEPTH, false>), grid, block,
                            0, s, a);
     return hipGetLastError();
 }
@@ -1018,7 +1018,7 @@ static hipError_t launch_dma_one(const ConvGemmArgs& a, hipStream_t s)
         hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
     if (attr != hipSuccess)
         return attr;
-    hipLaunchKernelGGL((conv_gemm_dma<T, BM, BN, WM, WN, NS, TAPV>),
+    PPIPE_LAUNCH((conv_gemm_dma<T, BM, BN, WM, WN, NS, TAPV>),
                        dim3((unsigned)(a.tiles_m * a.tiles_co * a.splits)), dim3(WM * WN * 64),
                        bytes, s, a);
     return hipGetLastError();
@@ -1037,14 +1037,14 @@ static hipError_t launch_skinny(int wk, const ConvGemmArgs& a, hipStream_t s)
     dim3 grid((unsigned)(a.tiles_m * a.tiles_co));
     switch (wk) {
     case 4:
-        hipLaunchKernelGGL((conv_gemm_skinny<T, FM, FN, 4, 8>), grid, dim3(256), 0, s, a);
+        PPIPE_LAUNCH((conv_gemm_skinny<T, FM, FN, 4, 8>), grid, dim3(256), 0, s, a);
         break;
     case 8:
-        hipLaunchKernelGGL((conv_gemm_skinny<T, FM, FN, 8, 8>), grid, dim3(512), 0, s, a);
+        PPIPE_LAUNCH((conv_gemm_skinny<T, FM, FN, 8, 8>), grid, dim3(512), 0, s, a);
         break;
     case 16:   // 1024 threads: only the 16x16 tile fits the register file
         if constexpr (FM * FN == 1) {
-            hipLaunchKernelGGL((conv_gemm_skinny<T, FM, FN, 16, 8>), grid, dim3(1024), 0, s, a);
+            PPIPE_LAUNCH((conv_gemm_skinny<T, FM, FN, 16, 8>), grid, dim3(1024), 0, s, a);
             break;
         }
         return hipErrorInvalidValue;
@@ -1094,13 +1094,13 @@ hipError_t launch_softmax_rows(const float* z, int splits, const float* scale, c
 {
     static_assert(SOFTMAX_MAX_O <= 256 * 32, "row fits the register array");
     if (O <= 1024)
-        hipLaunchKernelGGL(softmax_rows_kernel<4>, dim3(M), dim3(256), 0, s, z, splits, scale,
+        PPIPE_LAUNCH(softmax_rows_kernel<4>, dim3(M), dim3(256), 0, s, z, splits, scale,
                            bias, M, O, out);
     else if (O <= 2048)
-        hipLaunchKernelGGL(softmax_rows_kernel<8>, dim3(M), dim3(256), 0, s, z, splits, scale,
+        PPIPE_LAUNCH(softmax_rows_kernel<8>, dim3(M), dim3(256), 0, s, z, splits, scale,
                            bias, M, O, out);
     else if (O <= SOFTMAX_MAX_O)
-        hipLaunchKernelGGL(softmax_rows_kernel<32>, dim3(M), dim3(256), 0, s, z, splits, scale,
+        PPIPE_LAUNCH(softmax_rows_kernel<32>, dim3(M), dim3(256), 0, s, z, splits, scale,
                            bias, M, O, out);
     else
         return hipErrorInvalidValue;
@@ -1115,13 +1115,13 @@ hipError_t launch_splitk_reduce(int dt, const ConvGemmArgs& a, hipStream_t s)
     const dim3 grid((unsigned)((nvec + 255) / 256)), block(256);
     switch (dt) {
     case DT_F32:
-        hipLaunchKernelGGL(splitk_reduce_kernel<float>, grid, block, 0, s, a);
+        PPIPE_LAUNCH(splitk_reduce_kernel<float>, grid, block, 0, s, a);
         break;
     case DT_F16:
-        hipLaunchKernelGGL(splitk_reduce_kernel<_Float16>, grid, block, 0, s, a);
+        PPIPE_LAUNCH(splitk_reduce_kernel<_Float16>, grid, block, 0, s, a);
         break;
     case DT_BF16:
-        hipLaunchKernelGGL(splitk_reduce_kernel<__bf16>, grid, block, 0, s, a);
+        PPIPE_LAUNCH(splitk_reduce_kernel<__bf16>, grid, block, 0, s, a);
         break;
     default:
         return hipErrorInvalidValue;

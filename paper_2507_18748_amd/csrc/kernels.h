@@ -2,12 +2,31 @@
 // Not part of the public ABI (include/ppipe.h is).
 #pragma once
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <cstddef>
 #include <cstdint>
 
 namespace ppipe {
 
 enum DType : int { DT_F32 = 0, DT_F16 = 1, DT_BF16 = 2 };
+
+// Timing events for the next kernel launch of this host thread (set by the
+// runtime's timed runs, null otherwise).  With events set, launches go
+// through hipExtLaunchKernelGGL, which records them around the kernel itself.
+struct LaunchEvents {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchEvents& launch_events();
+
+#define PPIPE_LAUNCH(KERNEL, GRID, BLOCK, SHMEM, STREAM, ...)                                   \
+    do {                                                                                         \
+        const ::ppipe::LaunchEvents ev_ = ::ppipe::launch_events();                              \
+        if (ev_.start)                                                                           \
+            hipExtLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, ev_.start, ev_.stop, 0u,   \
+                                  __VA_ARGS__);                                                  \
+        else                                                                                     \
+            hipLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, __VA_ARGS__);                 \
+    } while (0)
 enum Act : int { ACT_NONE = 0, ACT_RELU = 1, ACT_RELU6 = 2 };
 
 inline int dtype_size(int dt) { return dt == DT_F32 ? 4 : 2; }

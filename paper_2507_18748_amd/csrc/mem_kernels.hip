@@ -225,7 +225,7 @@ hipError_t launch_dwconv(int dt, const void* x, const void* w, const float* scal
     if (k != 3)
         return hipErrorInvalidValue;
     const size_t total = (size_t)N * Ho * Wo * C / (16 / dtype_size(dt));
-    PPIPE_DISPATCH(dt, hipLaunchKernelGGL((dwconv_kernel<T, 3>), dim3(blocks_for(total)),
+    PPIPE_DISPATCH(dt, PPIPE_LAUNCH((dwconv_kernel<T, 3>), dim3(blocks_for(total)),
                                           dim3(256), 0, s, (const T*)x, (const T*)w, scale,
                                           bias, (T*)y, N, H, W, C, Ho, Wo, stride, pad, act));
     return hipGetLastError();
@@ -235,7 +235,7 @@ hipError_t launch_maxpool(int dt, const void* x, void* y, int N, int H, int W, i
                           int Ho, int Wo, int k, int stride, int pad, hipStream_t s)
 {
     const size_t total = (size_t)N * Ho * Wo * C / (16 / dtype_size(dt));
-    PPIPE_DISPATCH(dt, hipLaunchKernelGGL(maxpool_kernel<T>, dim3(blocks_for(total)),
+    PPIPE_DISPATCH(dt, PPIPE_LAUNCH(maxpool_kernel<T>, dim3(blocks_for(total)),
                                           dim3(256), 0, s, (const T*)x, (T*)y, N, H, W, C,
                                           Ho, Wo, k, stride, pad));
     return hipGetLastError();
@@ -245,7 +245,7 @@ hipError_t launch_gap(int dt, const void* x, void* y, int N, int HW, int C, hipS
 {
     const int CV = C / (16 / dtype_size(dt));
     const unsigned blocks = (unsigned)N * ((CV + 31) / 32);
-    PPIPE_DISPATCH(dt, hipLaunchKernelGGL(gap_kernel<T>, dim3(blocks), dim3(256), 0, s,
+    PPIPE_DISPATCH(dt, PPIPE_LAUNCH(gap_kernel<T>, dim3(blocks), dim3(256), 0, s,
                                           (const T*)x, (T*)y, N, HW, C));
     return hipGetLastError();
 }
@@ -253,7 +253,7 @@ hipError_t launch_gap(int dt, const void* x, void* y, int N, int HW, int C, hipS
 hipError_t launch_pad_channels(int dt, const void* x, void* y, size_t npix, int C, int Cp,
                                hipStream_t s)
 {
-    PPIPE_DISPATCH(dt, hipLaunchKernelGGL(pad_channels_kernel<T>, dim3(blocks_for(npix)),
+    PPIPE_DISPATCH(dt, PPIPE_LAUNCH(pad_channels_kernel<T>, dim3(blocks_for(npix)),
                                           dim3(256), 0, s, (const T*)x, (T*)y, npix, C, Cp));
     return hipGetLastError();
 }
@@ -266,7 +266,7 @@ const char* pad_channels_name(int dt)
 
 hipError_t launch_fill_uniform(int dt, void* p, size_t n, uint32_t seed, hipStream_t s)
 {
-    PPIPE_DISPATCH(dt, hipLaunchKernelGGL(fill_uniform_kernel<T>, dim3(blocks_for(n)),
+    PPIPE_DISPATCH(dt, PPIPE_LAUNCH(fill_uniform_kernel<T>, dim3(blocks_for(n)),
                                           dim3(256), 0, s, (T*)p, n, seed));
     return hipGetLastError();
 }

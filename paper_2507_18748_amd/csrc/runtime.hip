@@ -138,7 +138,21 @@ struct ppipe_partition {
     std::vector<uint8_t> host_blob;   // packed parameters between validation and upload
     hipStream_t cap_stream = nullptr;
     std::vector<GraphEntry> graphs;
+    // timed runs: an event before and after every launch of one run
+    struct {
+        int batch = 0;
+        const void* in = nullptr;
+        void* out = nullptr;
+        std::vector<hipEvent_t> ev;
+        bool ran = false;
+    } timed;
 };
+
+LaunchEvents& ppipe::launch_events()
+{
+    thread_local LaunchEvents ev;
+    return ev;
+}
 
 namespace {
 
@@ -240,6 +254,24 @@ struct LaunchHook {
     virtual ~LaunchHook() = default;
     virtual void before(const LayerRT&, int, hipStream_t) {}
     virtual void after(const LayerRT&, int, hipStream_t) {}
+};
+
+// Hands the k-th event pair to the k-th launch of a run (the launch records
+// them around the kernel itself).
+struct TimedHook : LaunchHook {
+    explicit TimedHook(const std::vector<hipEvent_t>& e) : ev(e) {}
+    ~TimedHook() override { launch_events() = LaunchEvents{}; }
+    const std::vector<hipEvent_t>& ev;
+    size_t k = 0;
+    void before(const LayerRT&, int, hipStream_t) override
+    {
+        if (2 * k + 1 < ev.size()) launch_events() = LaunchEvents{ev[2 * k], ev[2 * k + 1]};
+    }
+    void after(const LayerRT&, int, hipStream_t) override
+    {
+        launch_events() = LaunchEvents{};
+        ++k;
+    }
 };
 
 // Launch sequence of a GEMM layer: [channel pad], GEMM, [split-K reduce], [softmax].
@@ -426,8 +458,17 @@ int ensure_device(const ppipe_partition* P)
     return PPIPE_OK;
 }
 
+void release_timed(ppipe_partition* P)
+{
+    for (hipEvent_t e : P->timed.ev) (void)hipEventDestroy(e);
+    P->timed.ev.clear();
+    P->timed.batch = 0;
+    P->timed.ran = false;
+}
+
 void release(ppipe_partition* P)
 {
+    release_timed(P);
     for (GraphEntry& g : P->graphs) {
         (void)hipGraphExecDestroy(g.exec);
         (void)hipGraphDestroy(g.graph);
@@ -1048,6 +1089,74 @@ int ppipe_profile_kernels(ppipe_partition* h, int32_t batch, int32_t warmup, int
             rec.min_us = *std::min_element(t.begin(), t.end());
         }
     }
+    return PPIPE_OK;
+}
+
+int ppipe_timing_setup(ppipe_partition* h, int32_t batch, const void* in, void* out)
+{
+    int rc = check_run_args(h, batch, in, out);
+    if (rc != PPIPE_OK) return rc;
+    if ((rc = ensure_device(h)) != PPIPE_OK) return rc;
+    (void)hipDeviceSynchronize();
+    release_timed(h);
+    int nlaunch = 0;
+    for (const LayerRT& l : h->L) nlaunch += layer_launches(l, batch);
+    h->timed.ev.assign(2 * (size_t)nlaunch, nullptr);
+    for (hipEvent_t& e : h->timed.ev) {
+        const hipError_t he = hipEventCreate(&e);
+        if (he != hipSuccess) {
+            release_timed(h);
+            return fail(PPIPE_E_HIP, hip_msg("hipEventCreate", he));
+        }
+    }
+    h->timed.batch = batch;
+    h->timed.in = in;
+    h->timed.out = out;
+    return PPIPE_OK;
+}
+
+int ppipe_partition_run_timed(ppipe_partition* h, void* stream)
+{
+    if (!h) return fail(PPIPE_E_INVALID, "null partition handle");
+    if (h->timed.batch < 1) return fail(PPIPE_E_INVALID, "ppipe_timing_setup was not called");
+    int rc = ensure_device(h);
+    if (rc != PPIPE_OK) return rc;
+    TimedHook hook(h->timed.ev);
+    const hipError_t e = enqueue_all(h, h->timed.batch, h->timed.in, h->timed.out,
+                                     (hipStream_t)stream, &hook);
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("timed run", e));
+    h->timed.ran = true;
+    return PPIPE_OK;
+}
+
+int ppipe_timing_read(ppipe_partition* h, ppipe_kernel_record* records, int32_t capacity,
+                      int32_t* count)
+{
+    if (!h || !count) return fail(PPIPE_E_INVALID, "null argument");
+    if (!h->timed.ran) return fail(PPIPE_E_INVALID, "no timed run since ppipe_timing_setup");
+    int rc = ensure_device(h);
+    if (rc != PPIPE_OK) return rc;
+    hipError_t e = hipEventSynchronize(h->timed.ev.back());
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipEventSynchronize", e));
+    const int batch = h->timed.batch;
+    int k = 0;
+    for (const LayerRT& l : h->L) {
+        for (int j = 0; j < layer_launches(l, batch); ++j, ++k) {
+            if (!records || k >= capacity) continue;
+            float ms = 0;
+            e = hipEventElapsedTime(&ms, h->timed.ev[2 * k], h->timed.ev[2 * k + 1]);
+            if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipEventElapsedTime", e));
+            ppipe_kernel_record& rec = records[k];
+            std::memset(&rec, 0, sizeof(rec));
+            rec.layer = l.index;
+            rec.launch = j;
+            std::snprintf(rec.kernel, sizeof(rec.kernel), "%s",
+                          launch_name(h, l, batch, j).c_str());
+            launch_work(h, l, batch, j, &rec.flops, &rec.bytes);
+            rec.mean_us = rec.median_us = rec.min_us = ms * 1000.0f;
+        }
+    }
+    *count = k;
     return PPIPE_OK;
 }
 

@@ -107,3 +107,14 @@ def test_create_rejects_bad_descriptions():
     miss = _params(L)
     del miss[2]["weight"]
     assert _status_of(lambda: Partition(L, miss, (8, 9, 9), 0, 5, "f16")) == -1
+
+
+def test_timing_calls_reject_a_null_handle():
+    """Error paths of the timed-run entry points need no device."""
+    import ctypes
+    from paper_2507_18748_amd.binding import load_library, KernelRecord
+    lib = load_library()
+    n = ctypes.c_int32(0)
+    assert lib.ppipe_partition_run_timed(None, None) == -1
+    assert lib.ppipe_timing_read(None, (KernelRecord * 1)(), 1, ctypes.byref(n)) == -1
+    assert lib.ppipe_timing_setup(None, 1, None, None) == -1

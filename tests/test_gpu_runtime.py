@@ -39,6 +39,32 @@ def test_bitwise_repeatable_and_graph_replay_matches_eager():
             np.testing.assert_array_equal(got, a)
 
 
+def test_timed_runs_match_plain_runs_and_time_every_launch():
+    """Timed runs (events recorded by every launch) give the same bits as
+    plain runs, and one record per launch with a positive duration."""
+    import torch
+    from paper_2507_18748_amd import Partition
+    wl, m, P = _small()
+    x = wl.input(8)
+    with Partition(m.layers, P, (3, 224, 224), wl.begin, wl.end, wl.dtype, max_batch=8) as part:
+        ref = gpu_forward(part, x)
+        xd = upload_nhwc(x, wl.dtype)
+        out = empty_out(part, 8)
+        part.timing_setup(8, xd.data_ptr(), out.data_ptr())
+        s = torch.cuda.current_stream().cuda_stream
+        for _ in range(3):
+            out.zero_()
+            part.run_timed(s)
+            torch.cuda.synchronize()
+            got = out.float().cpu().numpy().transpose(0, 3, 1, 2)
+            np.testing.assert_array_equal(got, ref)
+        recs = part.timing_read()
+        launches = sum(part.layer_info(i, 8)["kernel_count"] for i in range(wl.begin, wl.end))
+        assert len(recs) == launches
+        assert all(r["mean_us"] > 0 for r in recs)
+        assert [r["layer"] for r in recs] == sorted(r["layer"] for r in recs)
+
+
 def test_batch_sweep_on_one_handle():
     from paper_2507_18748_amd import Partition
     wl, m, P = _small()
