@@ -931,18 +931,29 @@ softmax_rows_kernel(const float* __restrict__ z, int splits, const float* __rest
     const int m = blockIdx.x;
     const size_t plane = (size_t)M * O;
     const float* zr = z + (size_t)m * O;
+    // Split sums in split order; the loads of up to four splits are issued
+    // before their additions so that the row's memory latency overlaps.
     float v[VPT];
 #pragma unroll
     for (int q = 0; q < VPT; ++q) {
         const int o = t + q * 256;
         v[q] = o < O ? zr[o] : 0.0f;
     }
-    for (int sp = 1; sp < splits; ++sp)
+    for (int sp0 = 1; sp0 < splits; sp0 += 4) {
+        float u[4][VPT];
 #pragma unroll
-        for (int q = 0; q < VPT; ++q) {
-            const int o = t + q * 256;
-            if (o < O) v[q] += zr[sp * plane + o];
-        }
+        for (int d = 0; d < 4; ++d)
+#pragma unroll
+            for (int q = 0; q < VPT; ++q) {
+                const int o = t + q * 256;
+                u[d][q] = (sp0 + d < splits && o < O) ? zr[(sp0 + d) * plane + o] : 0.0f;
+            }
+#pragma unroll
+        for (int d = 0; d < 4; ++d)
+#pragma unroll
+            for (int q = 0; q < VPT; ++q)
+                if (sp0 + d < splits) v[q] += u[d][q];
+    }
     float mx = -INFINITY;
 #pragma unroll
     for (int q = 0; q < VPT; ++q) {

@@ -52,49 +52,114 @@ __device__ __forceinline__ float act_f(float v, int act)
 }
 
 // y[n][ho][wo][c] = act(scale[c] * sum_{kh,kw} x[n][ho*s-p+kh][wo*s-p+kw][c] * w[kh][kw][c] + bias[c])
-template <typename T, int K>
+//
+// 3x3 depthwise, stride S: each thread owns one 16-byte channel vector of PW
+// consecutive output pixels of one row, so an input column is loaded once for
+// every output that uses it and the nine weight vectors once per PW outputs.
+// All loads are buffer loads issued without branches: taps outside the image
+// use an offset beyond the buffer and read zeros.  Consecutive lanes take
+// consecutive channel vectors (coalesced 16-byte accesses).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t dw_rsrc(const void* p, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes,
+                                             0x00020000);
+}
+__device__ __forceinline__ uint4 dw_load(__amdgpu_buffer_rsrc_t r, uint32_t off)
+{
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+template <typename T>
+__device__ __forceinline__ void unpack16(const uint4& u, float* f)
+{
+    if constexpr (sizeof(T) == 4) {
+        f[0] = __uint_as_float(u.x); f[1] = __uint_as_float(u.y);
+        f[2] = __uint_as_float(u.z); f[3] = __uint_as_float(u.w);
+    } else {
+        T e[8];
+        __builtin_memcpy(e, &u, 16);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) f[i] = (float)e[i];
+    }
+}
+
+template <typename T, int S, int PW>
 __global__ void __launch_bounds__(256)
-dwconv_kernel(const T* __restrict__ x, const T* __restrict__ w, const float* __restrict__ scale,
-              const float* __restrict__ bias, T* __restrict__ y, int N, int H, int W, int C,
-              int Ho, int Wo, int stride, int pad, int act)
+dwconv3_kernel(const T* __restrict__ x, const T* __restrict__ w, const float* __restrict__ scale,
+               const float* __restrict__ bias, T* __restrict__ y, int N, int H, int W, int C,
+               int Ho, int Wo, int pad, int act)
 {
     constexpr int V = Vec16<T>::N;
+    constexpr int ESZ = (int)sizeof(T);
+    constexpr int NCOL = (PW - 1) * S + 3;     // input columns one row of PW outputs reads
+    constexpr uint32_t OOB = 0x80000000u;
     const int CV = C / V;
-    const size_t total = (size_t)N * Ho * Wo * CV;
-    const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int WQ = (Wo + PW - 1) / PW;
+    const uint32_t total = (uint32_t)N * Ho * WQ * CV;
+    const uint32_t idx = blockIdx.x * 256u + threadIdx.x;
     if (idx >= total)
         return;
     const int cv = (int)(idx % CV);
-    size_t p = idx / CV;
-    const int wo = (int)(p % Wo);
-    p /= Wo;
-    const int ho = (int)(p % Ho);
-    const int n = (int)(p / Ho);
-    const int c = cv * V;
-    float acc[V];
+    uint32_t t = idx / CV;
+    const int wq = (int)(t % WQ);
+    t /= WQ;
+    const int ho = (int)(t % Ho);
+    const int n = (int)(t / Ho);
+    const int c = cv * V, wo0 = wq * PW;
+    const auto xr = dw_rsrc(x, (uint32_t)N * H * W * C * ESZ);
+    const auto wr = dw_rsrc(w, 9u * C * ESZ);
+
+    uint4 wk[9];
 #pragma unroll
-    for (int i = 0; i < V; ++i) acc[i] = 0.0f;
+    for (int q = 0; q < 9; ++q)
+        wk[q] = dw_load(wr, (uint32_t)(q * C + c) * ESZ);
+
+    float acc[PW][V];
 #pragma unroll
-    for (int kh = 0; kh < K; ++kh) {
-        const int hi = ho * stride - pad + kh;
-        if ((unsigned)hi >= (unsigned)H)
-            continue;
+    for (int p = 0; p < PW; ++p)
 #pragma unroll
-        for (int kw = 0; kw < K; ++kw) {
-            const int wi = wo * stride - pad + kw;
-            if ((unsigned)wi >= (unsigned)W)
-                continue;
-            float xv[V], wv[V];
-            Vec16<T>::load(x + (((size_t)n * H + hi) * W + wi) * C + c, xv);
-            Vec16<T>::load(w + (size_t)(kh * K + kw) * C + c, wv);
+        for (int i = 0; i < V; ++i) acc[p][i] = 0.0f;
+
+    const int wi0 = wo0 * S - pad;
 #pragma unroll
-            for (int i = 0; i < V; ++i) acc[i] = fmaf(xv[i], wv[i], acc[i]);
+    for (int kh = 0; kh < 3; ++kh) {
+        const int hi = ho * S - pad + kh;
+        const bool hok = (unsigned)hi < (unsigned)H;
+        const uint32_t row = (uint32_t)(((n * H + hi) * W) * C + c) * ESZ;
+        uint4 xc[NCOL];
+#pragma unroll
+        for (int j = 0; j < NCOL; ++j) {
+            const int wi = wi0 + j;
+            const bool ok = hok && (unsigned)wi < (unsigned)W;
+            xc[j] = dw_load(xr, ok ? row + (uint32_t)(wi * C * ESZ) : OOB);
+        }
+#pragma unroll
+        for (int kw = 0; kw < 3; ++kw) {
+            float wf[V];
+            unpack16<T>(wk[kh * 3 + kw], wf);
+#pragma unroll
+            for (int p = 0; p < PW; ++p) {
+                float xf[V];
+                unpack16<T>(xc[p * S + kw], xf);
+#pragma unroll
+                for (int i = 0; i < V; ++i) acc[p][i] = fmaf(xf[i], wf[i], acc[p][i]);
+            }
         }
     }
-    float o[V];
+    float sc[V], bi[V];
 #pragma unroll
-    for (int i = 0; i < V; ++i) o[i] = act_f(acc[i] * scale[c + i] + bias[c + i], act);
-    Vec16<T>::store(y + (((size_t)n * Ho + ho) * Wo + wo) * C + c, o);
+    for (int i = 0; i < V; ++i) {
+        sc[i] = scale[c + i];
+        bi[i] = bias[c + i];
+    }
+#pragma unroll
+    for (int p = 0; p < PW; ++p) {
+        if (wo0 + p >= Wo)
+            break;
+        float o[V];
+#pragma unroll
+        for (int i = 0; i < V; ++i) o[i] = act_f(acc[p][i] * sc[i] + bi[i], act);
+        Vec16<T>::store(y + ((size_t)(n * Ho + ho) * Wo + wo0 + p) * C + c, o);
+    }
 }
 
 template <typename T>
@@ -222,12 +287,22 @@ hipError_t launch_dwconv(int dt, const void* x, const void* w, const float* scal
                          const float* bias, void* y, int N, int H, int W, int C, int Ho,
                          int Wo, int k, int stride, int pad, int act, hipStream_t s)
 {
-    if (k != 3)
+    if (k != 3 || (stride != 1 && stride != 2))
         return hipErrorInvalidValue;
-    const size_t total = (size_t)N * Ho * Wo * C / (16 / dtype_size(dt));
-    PPIPE_DISPATCH(dt, PPIPE_LAUNCH((dwconv_kernel<T, 3>), dim3(blocks_for(total)),
-                                          dim3(256), 0, s, (const T*)x, (const T*)w, scale,
-                                          bias, (T*)y, N, H, W, C, Ho, Wo, stride, pad, act));
+    const int cv = C / (16 / dtype_size(dt));
+    const int pw = stride == 1 ? 4 : 2;
+    const size_t total = (size_t)N * Ho * ((Wo + pw - 1) / pw) * cv;
+    if (total >= (1u << 31) || (double)N * H * W * C * dtype_size(dt) >= 2147483648.0)
+        return hipErrorInvalidValue;
+    if (stride == 1) {
+        PPIPE_DISPATCH(dt, PPIPE_LAUNCH((dwconv3_kernel<T, 1, 4>), dim3(blocks_for(total)),
+                                        dim3(256), 0, s, (const T*)x, (const T*)w, scale,
+                                        bias, (T*)y, N, H, W, C, Ho, Wo, pad, act));
+    } else {
+        PPIPE_DISPATCH(dt, PPIPE_LAUNCH((dwconv3_kernel<T, 2, 2>), dim3(blocks_for(total)),
+                                        dim3(256), 0, s, (const T*)x, (const T*)w, scale,
+                                        bias, (T*)y, N, H, W, C, Ho, Wo, pad, act));
+    }
     return hipGetLastError();
 }
 

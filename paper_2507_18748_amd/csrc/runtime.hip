@@ -167,23 +167,28 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok)
         return (int64_t)((M + c.bn - 1) / c.bn) * ((Co + c.bm - 1) / c.bm);
     };
     auto steps = [&](int cfg) { return (K + gemm_bk(cfg, dt) - 1) / gemm_bk(cfg, dt); };
-    // Measured on MI355X over the layers of the five partition workloads:
-    // 8-wave 128x128 tiles win once there are enough of them to fill the chip
-    // (or, with a long K loop, a hundred of them split over K); 64x64 tiles win
-    // everywhere else.  Splitting K pays for the extra reduction pass only when
-    // each split keeps several K steps, and only while the grid is short of
-    // about two blocks per CU.
-    // Both families stage operands with LDS-direct loads.  Dense grids take
-    // the two-stage loop (lowest registers and LDS, highest occupancy); sparse
-    // grids (under two 64x64 blocks, or one 8-wave block, per CU) take the
-    // software-pipelined loop.
+    // Fitted to per-layer sweeps of every plan over the five partition
+    // workloads on MI355X, timed in layer order (weights cold as in a real
+    // run, the split-K reduction at its in-order cost of ~4 us):
+    //  * 16-bit layers with Co >= 128 take 8-wave 128x128 tiles once there
+    //    are enough of them to fill the chip, or, with a long K loop, a
+    //    hundred of them split over K;
+    //  * everything else takes 64x64 tiles, splitting K only while the grid
+    //    is short of about 1.5 blocks per CU and each split keeps >= 4 steps;
+    //  * sparse grids (under two 64x64 blocks, or one 8-wave block, per CU)
+    //    take the software-pipelined three-stage loop, dense grids the
+    //    two-stage loop (fewest registers and LDS, highest occupancy);
+    //  * small fp32 layers take the skinny kernel (no reduction pass).
     const bool wide = dt != PPIPE_F32 && Co >= 128;
     const int64_t t128 = tiles(GEMM_DMA_128x128_8W_S2);
     const int k128 = steps(GEMM_DMA_128x128_8W_S2);
     int cfg = GEMM_DMA_64x64_S2, wk = 0, splits = 1;
-    if (wide && (t128 >= 192 || (t128 >= 96 && k128 >= 64))) {
+    if (dt == PPIPE_F32 && skinny_ok && M <= 4096 && K >= 256) {
+        cfg = GEMM_SK_32x32;
+        wk = 4;
+    } else if (wide && (t128 >= 384 || (t128 >= 96 && k128 >= 64))) {
         cfg = GEMM_DMA_128x128_8W_S2;
-        if (t128 < 192)
+        if (t128 < 384)
             while (splits < 16 && t128 * splits * 2 <= 512 && k128 / (splits * 2) >= 8)
                 splits *= 2;
         if (t128 * splits < 256)
@@ -194,7 +199,7 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok)
         while (splits < 32) {
             const int64_t nb = t * splits * 2;
             const int cps = k / (splits * 2);
-            const bool ok = splits == 1 ? (cps >= 4 && (nb <= 384 || (nb <= 512 && cps >= 8)))
+            const bool ok = splits == 1 ? (cps >= 4 && nb <= 384)
                                         : ((nb <= 128 && cps >= 2) || (nb <= 384 && cps >= 4) ||
                                            (nb <= 512 && cps >= 8));
             if (!ok) break;
@@ -590,9 +595,13 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
         if (ld.op == PPIPE_OP_CONV && ld.groups > 1) {
             if (!(ld.groups == ld.c_in && ld.c_in == ld.c_out))
                 return fail(PPIPE_E_UNSUPPORTED, who + ": grouped conv other than depthwise");
-            if (ld.k != 3 || x.c % epv || ld.res_src >= 0)
-                return fail(PPIPE_E_UNSUPPORTED, who + ": depthwise kernel needs k = 3, C % " +
-                                                     std::to_string(epv) + " == 0, no residual");
+            if (ld.k != 3 || x.c % epv || ld.res_src >= 0 || (ld.stride != 1 && ld.stride != 2))
+                return fail(PPIPE_E_UNSUPPORTED, who + ": depthwise kernel needs k = 3, stride 1 "
+                                                     "or 2, C % " + std::to_string(epv) +
+                                                     " == 0, no residual");
+            // input is addressed with 32-bit byte offsets (buffer loads)
+            if ((double)P->max_batch * x.c * x.h * x.w * esz >= 2147483648.0)
+                return fail(PPIPE_E_UNSUPPORTED, who + ": input reaches 2 GiB at max_batch");
             if (!ld.weight)
                 return fail(PPIPE_E_INVALID, who + ": missing weight");
             l.kind = K_DW;

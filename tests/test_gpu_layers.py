@@ -95,9 +95,12 @@ def test_stem3x3_relu6_gather(dtype):
 
 @pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("stride", [1, 2])
-def test_depthwise3x3(dtype, stride):
-    check(make((96, 13, 13), [conv("dw", -1, 96, 96, 3, stride, 1, g=96, act="relu6")]),
-          dtype, 2)
+@pytest.mark.parametrize("chw", [(96, 13, 13), (24, 9, 11), (8, 5, 6), (40, 2, 3)])
+def test_depthwise3x3(dtype, stride, chw):
+    """Ragged output rows (the last pixel group of a row is partial), one and
+    several channel vectors, maps narrower than a pixel group."""
+    c = chw[0]
+    check(make(chw, [conv("dw", -1, c, c, 3, stride, 1, g=c, act="relu6")]), dtype, 2)
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
