@@ -105,6 +105,10 @@ def load_library() -> ctypes.CDLL:
     lib.ppipe_profile_kernels.restype = ctypes.c_int
     lib.ppipe_profile_kernels.argtypes = [vp, i32, i32, i32, ctypes.POINTER(KernelRecord), i32,
                                           ctypes.POINTER(i32)]
+    lib.ppipe_profile_kernels_cold.restype = ctypes.c_int
+    lib.ppipe_profile_kernels_cold.argtypes = [vp, i32, i32, ctypes.c_int64,
+                                               ctypes.POINTER(KernelRecord), i32,
+                                               ctypes.POINTER(i32)]
     lib.ppipe_timing_setup.restype = ctypes.c_int
     lib.ppipe_timing_setup.argtypes = [vp, i32, vp, vp]
     lib.ppipe_partition_run_timed.restype = ctypes.c_int
@@ -215,6 +219,16 @@ class Partition:
         recs = (KernelRecord * cap)()
         self._check(self._lib.ppipe_profile_kernels(self._h, batch, warmup, reps, recs, cap,
                                                     ctypes.byref(count)))
+        return _records(recs, count.value, cap)
+
+    def profile_kernels_cold(self, batch: int, reps: int = 10,
+                             sweep_bytes: int = 1 << 30) -> List[dict]:
+        """Isolated-cold per-launch timing (caches swept before every repetition)."""
+        count = ctypes.c_int32(0)
+        cap = 4 * (self.end - self.begin) + 8
+        recs = (KernelRecord * cap)()
+        self._check(self._lib.ppipe_profile_kernels_cold(self._h, batch, reps, sweep_bytes,
+                                                         recs, cap, ctypes.byref(count)))
         return _records(recs, count.value, cap)
 
     # --- launch timing inside runs ---

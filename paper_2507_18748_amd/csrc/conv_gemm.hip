@@ -532,6 +532,12 @@ __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, u
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                  :: "s"(lds), "v"(voff), "s"(r) : "memory");
 }
+// Workgroup barrier without the memory fence of __syncthreads (which waits
+// for every outstanding LDS read first).  Used where the LDS data a barrier
+// protects was written by LDS-direct loads each wave already waited for, and
+// the only reads still in flight target a stage no load overwrites next.
+__device__ __forceinline__ void bare_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
 // Wait until at most N of this wave's vector memory operations are pending
 // (they complete in issue order).
 template <int N>
@@ -688,7 +694,7 @@ conv_gemm_dma(ConvGemmArgs a)
 #define PPIPE_DSTEP(s, XA, XB, YA, YB)                                                            \
     do {                                                                                          \
         dma_wait<(NS - 3) * PER>();   /* this wave's loads of stage s have landed */              \
-        __syncthreads();              /* ... and every wave's; stage s - 2 is consumed */         \
+        bare_barrier();               /* ... and every wave's; stage s - 2 is consumed */         \
         issue(lds0 + wr * STAGE);                                                                 \
         PPIPE_READ(dyn_smem + rd * STAGE, XA, XB);                                                \
         if ((s) > 0)                                                                              \
@@ -705,7 +711,8 @@ conv_gemm_dma(ConvGemmArgs a)
             issue(lds0);
             for (int s = 0; s < nst; ++s) {
                 dma_wait<0>();     // this wave's loads of stage s have landed
-                __syncthreads();   // ... and every wave's; stage s - 1 is consumed
+                bare_barrier();    // ... and every wave's; stage s - 1 is consumed (its
+                                   // fragments fed this wave's MFMAs)
                 issue(lds0 + ((s + 1) & 1) * STAGE);
                 const unsigned char* S = dyn_smem + (s & 1) * STAGE;
 #pragma unroll
@@ -1002,6 +1009,10 @@ GemmCfgInfo gemm_cfg_info(int cfg)
     case GEMM_DMA_64x64_S3: return {64, 64, 8, false, 3, 4};
     case GEMM_DMA_128x128_8W_S2: return {128, 128, 8, false, 2, 8};
     case GEMM_DMA_128x128_8W_S3: return {128, 128, 8, false, 3, 8};
+    case GEMM_DMA_64x64_8W_S2: return {64, 64, 8, false, 2, 8};
+    case GEMM_DMA_64x64_8W_S3: return {64, 64, 8, false, 3, 8};
+    case GEMM_DMA_64x64_8W_S4: return {64, 64, 8, false, 4, 8};
+    case GEMM_DMA_64x64_8W_S6: return {64, 64, 8, false, 6, 8};
     default:            return {0, 0, 0, false};
     }
 }
@@ -1085,6 +1096,10 @@ static hipError_t launch_cfg(int cfg, int wk, bool tapv, const ConvGemmArgs& a,
     case GEMM_DMA_64x64_S3: return launch_dma<T, 64, 64, 2, 2, 3>(tapv, a, s);
     case GEMM_DMA_128x128_8W_S2: return launch_dma<T, 128, 128, 2, 4, 2>(tapv, a, s);
     case GEMM_DMA_128x128_8W_S3: return launch_dma<T, 128, 128, 2, 4, 3>(tapv, a, s);
+    case GEMM_DMA_64x64_8W_S2: return launch_dma<T, 64, 64, 2, 4, 2>(tapv, a, s);
+    case GEMM_DMA_64x64_8W_S3: return launch_dma<T, 64, 64, 2, 4, 3>(tapv, a, s);
+    case GEMM_DMA_64x64_8W_S4: return launch_dma<T, 64, 64, 2, 4, 4>(tapv, a, s);
+    case GEMM_DMA_64x64_8W_S6: return launch_dma<T, 64, 64, 2, 4, 6>(tapv, a, s);
     default:            return hipErrorInvalidValue;
     }
 }

@@ -80,7 +80,11 @@ enum GemmCfg : int {
     GEMM_DMA_64x64_S3 = 10,       // 4 waves, 3 stages, software-pipelined
     GEMM_DMA_128x128_8W_S2 = 11,  // 8 waves, 64x32 per wave, 2 stages
     GEMM_DMA_128x128_8W_S3 = 12,  // 8 waves, 3 stages, software-pipelined
-    GEMM_NCFG = 13
+    GEMM_DMA_64x64_8W_S2 = 13,    // 8 waves, 32x16 per wave, 2 stages
+    GEMM_DMA_64x64_8W_S3 = 14,    // 8 waves, 3 stages, software-pipelined
+    GEMM_DMA_64x64_8W_S4 = 15,    // 8 waves, 4 stages (two in flight)
+    GEMM_DMA_64x64_8W_S6 = 16,    // 8 waves, 6 stages (four in flight; few blocks per CU)
+    GEMM_NCFG = 17
 };
 struct GemmCfgInfo {
     int bm, bn, kv;       // tile rows (co), columns (m); kv: 16-byte vectors of K per LDS stage
@@ -142,6 +146,11 @@ const char* maxpool_name(int dt);
 // Mean over H x W per (n, c), fp32 sum, NHWC in -> [N][C] out.
 hipError_t launch_gap(int dt, const void* x, void* y, int N, int HW, int C, hipStream_t s);
 const char* gap_name(int dt);
+
+// Read `buf` (all but its last 16 MiB, which receive one result per
+// thread): isolated-cold profiling, evicts L2 and the memory-side cache
+// before a timed launch.  bytes >= 32 MiB.
+hipError_t launch_cache_sweep(void* buf, size_t bytes, hipStream_t s);
 
 // Deterministic pseudo-random fill in [0, 1) for profiling inputs.
 hipError_t launch_fill_uniform(int dt, void* p, size_t n, uint32_t seed, hipStream_t s);

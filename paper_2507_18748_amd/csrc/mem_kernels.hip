@@ -273,7 +273,34 @@ __global__ void __launch_bounds__(256) fill_uniform_kernel(T* p, size_t n, uint3
     p[i] = (T)((float)(h >> 8) * (1.0f / 16777216.0f));
 }
 
+// Cache sweep: reads a buffer (grid-stride, 16 bytes per thread per step)
+// and writes one 16-byte result per thread at its end, so that the data of a
+// following launch is no longer in L2 or in the memory-side cache and the
+// sweep leaves almost no dirty lines behind to be written back during it.
+constexpr unsigned SWEEP_BLOCKS = 4096;
+__global__ void __launch_bounds__(256) sweep_kernel(const uint4* __restrict__ a,
+                                                    uint4* __restrict__ res, size_t n)
+{
+    uint4 acc = make_uint4(0u, 0u, 0u, 0u);
+    for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256) {
+        const uint4 v = a[i];
+        acc.x ^= v.x; acc.y ^= v.y; acc.z ^= v.z; acc.w ^= v.w;
+    }
+    res[(size_t)blockIdx.x * 256 + threadIdx.x] = acc;
+}
+
 static unsigned blocks_for(size_t n) { return (unsigned)((n + 255) / 256); }
+
+hipError_t launch_cache_sweep(void* buf, size_t bytes, hipStream_t s)
+{
+    const size_t res = (size_t)SWEEP_BLOCKS * 256 * 16;   // one 16-byte result per thread
+    if (bytes < 2 * res)
+        return hipErrorInvalidValue;
+    const size_t n = (bytes - res) / 16;
+    PPIPE_LAUNCH(sweep_kernel, dim3(SWEEP_BLOCKS), dim3(256), 0, s, (const uint4*)buf,
+                 (uint4*)((char*)buf + (bytes - res) / 16 * 16), n);
+    return hipGetLastError();
+}
 
 #define PPIPE_DISPATCH(dt, KERNEL_CALL)                                   \
     switch (dt) {                                                         \

@@ -173,11 +173,15 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok)
     //  * 16-bit layers with Co >= 128 take 8-wave 128x128 tiles once there
     //    are enough of them to fill the chip, or, with a long K loop, a
     //    hundred of them split over K;
-    //  * everything else takes 64x64 tiles, splitting K only while the grid
-    //    is short of about 1.5 blocks per CU and each split keeps >= 4 steps;
-    //  * sparse grids (under two 64x64 blocks, or one 8-wave block, per CU)
-    //    take the software-pipelined three-stage loop, dense grids the
-    //    two-stage loop (fewest registers and LDS, highest occupancy);
+    //  * everything else takes 64x64 tiles; K is split only when each half
+    //    keeps >= 12 steps, then while the grid is short of about 1.5 blocks
+    //    per CU and each split keeps >= 4 steps;
+    //  * sparse grids (under two 64x64 blocks, or one 8-wave 128x128 block,
+    //    per CU) take software-pipelined loops; sparse 64x64 grids use 8
+    //    waves and four stages (two in flight), because a lone block streams
+    //    every operand byte from beyond L2 and is bound by the bytes it keeps
+    //    in flight; dense grids take the two-stage loop (fewest registers and
+    //    LDS, highest occupancy);
     //  * small fp32 layers take the skinny kernel (no reduction pass).
     const bool wide = dt != PPIPE_F32 && Co >= 128;
     const int64_t t128 = tiles(GEMM_DMA_128x128_8W_S2);
@@ -199,14 +203,14 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok)
         while (splits < 32) {
             const int64_t nb = t * splits * 2;
             const int cps = k / (splits * 2);
-            const bool ok = splits == 1 ? (cps >= 4 && nb <= 384)
+            const bool ok = splits == 1 ? (cps >= 12 && nb <= 384)
                                         : ((nb <= 128 && cps >= 2) || (nb <= 384 && cps >= 4) ||
                                            (nb <= 512 && cps >= 8));
             if (!ok) break;
             splits *= 2;
         }
         if (t * splits < 512)
-            cfg = GEMM_DMA_64x64_S3;
+            cfg = GEMM_DMA_64x64_8W_S4;
     }
     // PPIPE_GEMM_PLAN="cfg,waves,splits" forces one configuration on every
     // eligible GEMM layer (tuning sweeps and kernel tests).
@@ -1083,6 +1087,67 @@ int ppipe_profile_kernels(ppipe_partition* h, int32_t batch, int32_t warmup, int
                     return enqueue_layer(h, l, batch, pb.in, pb.out, pb.s, nullptr, j);
                 }, t);
             if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("profile run", e));
+            if (!records || k >= capacity) continue;
+            ppipe_kernel_record& rec = records[k];
+            std::memset(&rec, 0, sizeof(rec));
+            rec.layer = l.index;
+            rec.launch = j;
+            std::snprintf(rec.kernel, sizeof(rec.kernel), "%s",
+                          launch_name(h, l, batch, j).c_str());
+            launch_work(h, l, batch, j, &rec.flops, &rec.bytes);
+            double sum = 0;
+            for (float v : t) sum += v;
+            rec.mean_us = (float)(sum / t.size());
+            rec.median_us = median_of(t);
+            rec.min_us = *std::min_element(t.begin(), t.end());
+        }
+    }
+    return PPIPE_OK;
+}
+
+int ppipe_profile_kernels_cold(ppipe_partition* h, int32_t batch, int32_t reps,
+                               int64_t sweep_bytes, ppipe_kernel_record* records,
+                               int32_t capacity, int32_t* count)
+{
+    if (!h) return fail(PPIPE_E_INVALID, "null partition handle");
+    if (batch < 1 || batch > h->max_batch || reps < 1 || !count || sweep_bytes < (32 << 20))
+        return fail(PPIPE_E_INVALID, "bad batch, reps, sweep size or count pointer");
+    int rc = ensure_device(h);
+    if (rc != PPIPE_OK) return rc;
+    int nlaunch = 0;
+    for (const LayerRT& l : h->L) nlaunch += layer_launches(l, batch);
+    *count = nlaunch;
+    ProfileBuffers pb;
+    if ((rc = setup_profile(h, pb)) != PPIPE_OK) return rc;
+    struct Sweep {
+        void* p = nullptr;
+        ~Sweep() { if (p) (void)hipFree(p); }
+    } sw;
+    hipError_t e = hipMalloc(&sw.p, (size_t)sweep_bytes);
+    if (e != hipSuccess) return fail(PPIPE_E_NOMEM, hip_msg("hipMalloc(sweep buffer)", e));
+    if ((e = hipMemsetAsync(sw.p, 0, (size_t)sweep_bytes, pb.s)) != hipSuccess)
+        return fail(PPIPE_E_HIP, hip_msg("hipMemsetAsync", e));
+    Events ev;
+    if ((e = ev.make()) != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipEventCreate", e));
+    // one warm run so that every buffer a launch reads holds its producer's data
+    if ((e = enqueue_all(h, batch, pb.in, pb.out, pb.s, nullptr)) != hipSuccess)
+        return fail(PPIPE_E_HIP, hip_msg("kernel launch", e));
+    int k = 0;
+    for (const LayerRT& l : h->L) {
+        for (int j = 0; j < layer_launches(l, batch); ++j, ++k) {
+            std::vector<float> t;
+            for (int r = 0; r < reps && e == hipSuccess; ++r) {
+                e = launch_cache_sweep(sw.p, (size_t)sweep_bytes, pb.s);
+                if (e != hipSuccess) break;
+                launch_events() = LaunchEvents{ev.a, ev.b};
+                e = enqueue_layer(h, l, batch, pb.in, pb.out, pb.s, nullptr, j);
+                launch_events() = LaunchEvents{};
+                if (e == hipSuccess) e = hipEventSynchronize(ev.b);
+                float ms = 0;
+                if (e == hipSuccess) e = hipEventElapsedTime(&ms, ev.a, ev.b);
+                t.push_back(ms * 1000.0f);
+            }
+            if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("cold profile run", e));
             if (!records || k >= capacity) continue;
             ppipe_kernel_record& rec = records[k];
             std::memset(&rec, 0, sizeof(rec));

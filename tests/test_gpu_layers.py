@@ -196,6 +196,10 @@ FORCED = [  # (configuration id, waves, splits): every kernel variant the planne
     ("10,0,1", "conv_gemm<", "64x64,kv8,dma3"), ("10,0,2", "conv_gemm<", "64x64,kv8,dma3"),
     ("11,0,1", "conv_gemm<", "128x128,kv8,8w,dma2"), ("11,0,4", "conv_gemm<", "128x128,kv8,8w,dma2"),
     ("12,0,1", "conv_gemm<", "128x128,kv8,8w,dma3"), ("12,0,2", "conv_gemm<", "128x128,kv8,8w,dma3"),
+    ("13,0,1", "conv_gemm<", "64x64,kv8,8w,dma2"), ("13,0,3", "conv_gemm<", "64x64,kv8,8w,dma2"),
+    ("14,0,1", "conv_gemm<", "64x64,kv8,8w,dma3"), ("14,0,2", "conv_gemm<", "64x64,kv8,8w,dma3"),
+    ("15,0,1", "conv_gemm<", "64x64,kv8,8w,dma4"), ("15,0,3", "conv_gemm<", "64x64,kv8,8w,dma4"),
+    ("16,0,1", "conv_gemm<", "64x64,kv8,8w,dma6"), ("16,0,2", "conv_gemm<", "64x64,kv8,8w,dma6"),
 ]
 FORCED_SHAPES = {  # ragged M and Co, padded 3x3 taps, a 1x1 with a K tail, an FC + softmax
     "3x3": ((64, 13, 13), [conv("c", -1, 64, 100, 3, 1, 1)], 3, "normal"),

@@ -97,3 +97,13 @@ def test_profile_tables():
         assert len(recs) >= 12 and all(r["mean_us"] > 0 for r in recs)
         info = part.layer_info(44, 8)
         assert info["out_bytes_b1"] == 512 * 14 * 14 * 2 and info["flops_b1"] > 0
+
+
+def test_isolated_cold_profile_records_every_launch():
+    from paper_2507_18748_amd import Partition
+    wl, m, P = _small()
+    with Partition(m.layers, P, (3, 224, 224), wl.begin, wl.end, wl.dtype, max_batch=8) as part:
+        recs = part.profile_kernels_cold(8, reps=2, sweep_bytes=64 << 20)
+        launches = sum(part.layer_info(i, 8)["kernel_count"] for i in range(wl.begin, wl.end))
+        assert len(recs) == launches
+        assert all(r["min_us"] > 0 and r["min_us"] <= r["median_us"] for r in recs)
