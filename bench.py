@@ -52,6 +52,51 @@ def roofline(records, dtype):
     return out
 
 
+def cold_summary(records, dtype):
+    """Roofline fractions from isolated-cold launches (caches swept before
+    every repetition): per kernel family, HBM fraction bytes-weighted
+    (sum of bytes / (peak x sum of time)) for memory-bound families and for
+    GEMM launches the roofline puts on HBM, MFMA fraction FLOP-weighted for
+    GEMM launches it puts on MFMA.  Launches moving < 16 MB are counted
+    separately as launch-bound."""
+    peak_f = PEAK_MFMA_TFLOPS[dtype] * 1e12
+    peak_b = PEAK_HBM_GBS * 1e9
+    fam = {}
+    for r in records:
+        name = r["kernel"].split("<")[0]
+        t = r["median_us"] * 1e-6
+        if name.startswith("conv_gemm"):
+            if r["flops"] / peak_f >= r["bytes"] / peak_b:
+                name = "conv_gemm (MFMA-bound launches)"
+            else:
+                name = "conv_gemm (HBM-bound launches)"
+        g = fam.setdefault(name, {"us": 0.0, "bytes": 0.0, "flops": 0.0, "launches": 0,
+                                  "small_launches": 0, "us_big": 0.0, "bytes_big": 0.0})
+        g["us"] += r["median_us"]
+        g["bytes"] += r["bytes"]
+        g["flops"] += r["flops"]
+        g["launches"] += 1
+        if r["bytes"] < 16e6:
+            g["small_launches"] += 1
+        else:
+            g["us_big"] += r["median_us"]
+            g["bytes_big"] += r["bytes"]
+    out = {}
+    for name, g in fam.items():
+        if g["us"] <= 0:
+            continue
+        d = {"us_per_step": round(g["us"], 2), "launches": g["launches"],
+             "launches_under_16MB": g["small_launches"]}
+        if "MFMA-bound" in name:
+            d["mfma_frac"] = g["flops"] / (g["us"] * 1e-6 * peak_f)
+        else:
+            d["hbm_frac"] = g["bytes"] / (g["us"] * 1e-6 * peak_b)
+            if g["us_big"] > 0:
+                d["hbm_frac_launches_over_16MB"] = g["bytes_big"] / (g["us_big"] * 1e-6 * peak_b)
+        out[name] = d
+    return out
+
+
 def source_digest():
     """sha256 over the kernel and runtime sources (any change invalidates
     HBM counters taken before it)."""
@@ -106,8 +151,9 @@ def parse_batches(spec):
 
 
 def latency_table(args):
-    """Per-layer latency table L[i][b] (microseconds, median of back-to-back
-    repetitions) of the workload's partition, with the feature-map size S_i,
+    """Per-layer latency table L[i][b] (microseconds, median over runs of the
+    range in layer order, events recorded by each layer's first and last
+    launch) of the workload's partition, with the feature-map size S_i,
     each layer's algorithmic work and roofline position, and the measured
     whole-partition latency next to the sum of its layers (the paper's
     planner assumes partition latency = sum of layer latencies)."""
@@ -155,14 +201,73 @@ def latency_table(args):
            "partition_us": {b: float(whole[j]) for j, b in enumerate(batches)},
            "sum_of_layers_us": {b: float(table[:, j].sum()) for j, b in enumerate(batches)},
            "images_per_s": {b: b / (whole[j] * 1e-6) for j, b in enumerate(batches)},
-           "method": "median of 3 trials of back-to-back repetitions between HIP events; "
-                     "partition = one captured HIP graph replayed",
+           "method": "layers: median over runs of the range in layer order, HIP events "
+                     "recorded by each layer's first and last kernel launch; partition: one "
+                     "captured HIP graph replayed back to back",
            "rows": rows}
     with open(args.table, "w") as f:
         json.dump(out, f, indent=1)
     print(json.dumps({"table": args.table, "workload": wl.name, "batches": len(batches),
                       "partition_us": out["partition_us"]}))
     part.close()
+
+
+def blocks_report(args):
+    """Pre-partitioning (Sec. 5.2) on the measured table: the workload's range
+    is grouped into about N blocks of equal latency at the planning batch,
+    each block is then profiled as a partition of its own at every batch (the
+    block-latency table the planner consumes), and two additivity checks are
+    reported: the sum of a block's layer latencies against the block measured
+    alone, and the sum of the blocks against the whole range measured."""
+    import numpy as np
+    import torch
+    import workloads as W
+    from paper_2507_18748_amd import Partition, split_points, prepartition
+    wl = W.workload(args.workload)
+    batches = parse_batches(args.batches)
+    plan_b = wl.batch if wl.batch in batches else batches[-1]
+    m = wl.build_model()
+    P = wl.params(m)
+    torch.cuda.set_device(0)
+    in_chw = (m.in_c, m.in_h, m.in_w)
+    with Partition(m.layers, P, in_chw, wl.begin, wl.end, wl.dtype,
+                   max_batch=max(batches)) as part:
+        table, whole = part.profile_layers(batches, warmup=3, reps=args.profile_reps)
+    print("[blocks] layer table done", file=sys.stderr, flush=True)
+    ok = split_points(m.layers)
+    local_ok = [1] + [ok[p] for p in range(wl.begin + 1, wl.end)] + [1]
+    jb = batches.index(plan_b)
+    bounds = [wl.begin + b for b in prepartition(
+        [float(v) for v in table[:, jb]], local_ok, args.blocks)]
+    blocks = []
+    for bb, be in zip(bounds, bounds[1:]):
+        with Partition(m.layers, P, in_chw, bb, be, wl.dtype, max_batch=max(batches)) as bp:
+            bt, bw = bp.profile_layers(batches, warmup=3, reps=args.profile_reps)
+        layer_sum = table[bb - wl.begin:be - wl.begin].sum(axis=0)
+        blocks.append({"layers": [bb, be],
+                       "block_us": {b: float(bw[j]) for j, b in enumerate(batches)},
+                       "sum_of_layers_us": {b: float(layer_sum[j]) for j, b in enumerate(batches)},
+                       "layers_over_block": {b: float(layer_sum[j] / bw[j])
+                                             for j, b in enumerate(batches)}})
+        print(f"[blocks] block [{bb},{be}) done", file=sys.stderr, flush=True)
+    sum_blocks = {b: sum(k["block_us"][b] for k in blocks) for b in batches}
+    target = float(table[:, jb].sum()) / args.blocks
+    out = {"workload": wl.name, "layers": [wl.begin, wl.end], "batches": batches,
+           "n_blocks_requested": args.blocks, "planning_batch": plan_b,
+           "target_block_us": target, "boundaries": bounds,
+           "block_us_at_planning_batch": [k["sum_of_layers_us"][plan_b] for k in blocks],
+           "whole_us": {b: float(whole[j]) for j, b in enumerate(batches)},
+           "sum_of_blocks_us": sum_blocks,
+           "blocks_over_whole": {b: sum_blocks[b] / float(whole[j])
+                                 for j, b in enumerate(batches)},
+           "blocks": blocks,
+           "method": "layer table in sequence (events recorded by each layer's first and "
+                     "last launch); blocks and the whole range as captured HIP graphs "
+                     "replayed back to back"}
+    with open(args.blocks_out, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps({"blocks": args.blocks_out, "boundaries": bounds,
+                      "blocks_over_whole": out["blocks_over_whole"]}))
 
 
 def main():
@@ -173,6 +278,13 @@ def main():
     ap.add_argument("--workload", default="resnet50_layer4_head")
     ap.add_argument("--batch", type=int, default=0, help="override the workload batch")
     ap.add_argument("--no-graph", action="store_true", help="launch kernels directly")
+    ap.add_argument("--blocks-out", default="", metavar="OUT.json",
+                    help="pre-partition the workload into --blocks blocks from its latency "
+                         "table and write block tables and additivity checks")
+    ap.add_argument("--blocks", type=int, default=10, help="N of the pre-partitioning")
+    ap.add_argument("--cold-reps", type=int, default=5,
+                    help="isolated-cold repetitions per launch (caches swept before each); "
+                         "0 skips")
     ap.add_argument("--timing-steps", type=int, default=20,
                     help="directly launched steps whose per-launch events give the roofline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -213,6 +325,8 @@ def main():
 
     if args.table:
         return latency_table(args)
+    if args.blocks_out:
+        return blocks_report(args)
 
     wl = W.workload(args.workload)
     if args.batch:
@@ -299,6 +413,9 @@ def main():
                    f" {wl.dtype} {wl.input_kind}", "graph": not args.no_graph},
         "roofline": roof,
     }
+    if args.cold_reps > 0:
+        cold = part.profile_kernels_cold(wl.batch, reps=args.cold_reps)
+        result["isolated_cold"] = cold_summary(cold, wl.dtype)
     if args.cpu_seconds > 0:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(wl, m, P, args.cpu_seconds)

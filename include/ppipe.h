@@ -152,12 +152,16 @@ int ppipe_partition_run(ppipe_partition* h, int32_t batch, const void* in,
 int ppipe_partition_capture(ppipe_partition* h, int32_t batch, const void* in,
                             void* out);
 
-/* Per-layer latency table: for each batch_sizes[j], `warmup` untimed runs,
- * then `reps` runs with a HIP event before every layer and after the last on
- * a private stream; out_us[i * n_batches + j] = median microseconds of layer
- * begin + i, out_partition_us[j] = median of the whole range timed without
- * the per-layer events (either output may be NULL).  Allocates its own input
- * and output buffers, synchronises internally.  Returns a status. */
+/* Per-layer latency table, in sequence: for each batch_sizes[j], `warmup`
+ * untimed runs, then `reps` runs of the range in layer order on a private
+ * stream, each layer's first kernel launch recording a HIP event before it
+ * and its last launch one after it (events recorded by the launches
+ * themselves, nothing between the kernels); out_us[i * n_batches + j] =
+ * median microseconds of layer begin + i over the runs.  out_partition_us[j]
+ * = median over three trials of the whole range replayed `reps` times back
+ * to back as one captured HIP graph (per replay).  Either output may be NULL.
+ * Allocates its own input and output buffers, synchronises internally.
+ * Returns a status. */
 int ppipe_profile_layers(ppipe_partition* h, const int32_t* batch_sizes,
                          int32_t n_batches, int32_t warmup, int32_t reps,
                          float* out_us, float* out_partition_us);
@@ -168,6 +172,38 @@ int ppipe_profile_layers(ppipe_partition* h, const int32_t* batch_sizes,
 int ppipe_profile_kernels(ppipe_partition* h, int32_t batch, int32_t warmup,
                           int32_t reps, ppipe_kernel_record* records,
                           int32_t capacity, int32_t* count);
+
+/* ---- pre-partitioning (host only, no device needed) ---- */
+
+/* Valid partition boundaries of a model: ok[p] (p = 0 .. n_layers) is 1 when
+ * a partition may start at layer p, i.e. every layer p, p+1, ... reads only
+ * layer p-1 or later (one feature map crosses the boundary, the problem
+ * statement's Y_bj); ok[0] = ok[n_layers] = 1.  `ok` holds n_layers + 1
+ * entries, caller-owned.  Returns a status. */
+int ppipe_split_points(const ppipe_model_desc* desc, int32_t* ok);
+
+/* DNN pre-partitioning (Sec. 5.2): from the first layer on, consecutive
+ * layers are grouped until the group's summed latency is as close as
+ * possible to 1/n_blocks of the whole model's; repeated until the last
+ * layer.  Groups end only at valid boundaries (split_ok as returned by
+ * ppipe_split_points); of equally close ends the earlier one is taken.
+ * layer_us: n_layers latencies (>= 0).  block_begin receives the first layer
+ * of every block and, after them, n_layers (capacity n_layers + 1); *n_out
+ * the number of blocks (close to n_blocks, not always equal).  Returns a
+ * status. */
+int ppipe_prepartition(const double* layer_us, const int32_t* split_ok, int32_t n_layers,
+                       int32_t n_blocks, int32_t* block_begin, int32_t* n_out);
+
+/* Isolated-cold per-launch timing at one batch: before each of `reps`
+ * repetitions of a launch, a sweep reads `sweep_bytes` of a private buffer
+ * (>= 32 MiB; 512 MiB or more evicts L2 and the 256 MB memory-side cache), so
+ * the launch finds its weights and activations in HBM only; the launch then
+ * records a pair of HIP events around its kernel.  Records as in
+ * ppipe_profile_kernels (mean, median, min over the repetitions).
+ * Allocates its own buffers, synchronises internally.  Returns a status. */
+int ppipe_profile_kernels_cold(ppipe_partition* h, int32_t batch, int32_t reps,
+                               int64_t sweep_bytes, ppipe_kernel_record* records,
+                               int32_t capacity, int32_t* count);
 
 /* Launch timing.  Prepares (batch, in, out) for ppipe_partition_run_timed:
  * every kernel launch of a timed run records a pair of HIP events around

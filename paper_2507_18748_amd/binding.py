@@ -122,6 +122,11 @@ def load_library() -> ctypes.CDLL:
     lib.ppipe_layer_info.argtypes = [vp, i32, i32, ctypes.POINTER(LayerInfo)]
     lib.ppipe_partition_destroy.restype = None
     lib.ppipe_partition_destroy.argtypes = [vp]
+    lib.ppipe_split_points.restype = ctypes.c_int
+    lib.ppipe_split_points.argtypes = [ctypes.POINTER(ModelDesc), ctypes.POINTER(i32)]
+    lib.ppipe_prepartition.restype = ctypes.c_int
+    lib.ppipe_prepartition.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32), i32,
+                                       i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
     lib.ppipe_last_error.restype = ctypes.c_char_p
     lib.ppipe_last_error.argtypes = []
     lib.ppipe_last_status.restype = ctypes.c_int32
@@ -136,6 +141,38 @@ def _err(lib, status: int):
 
 def _attr(L, name, default=None):
     return L[name] if isinstance(L, dict) else getattr(L, name, default)
+
+
+def split_points(layers: Sequence) -> List[int]:
+    """ok[p] for p = 0 .. len(layers): 1 when a partition may start at layer p
+    (ppipe_split_points)."""
+    lib = load_library()
+    arr = (LayerDesc * len(layers))()
+    for i, L in enumerate(layers):
+        arr[i].op = OPS[_attr(L, "op")]
+        arr[i].src = _attr(L, "src")
+        arr[i].res_src = _attr(L, "res_src", -1)
+    desc = ModelDesc(len(layers), arr, 0, 0, 0, 1)
+    ok = (ctypes.c_int32 * (len(layers) + 1))()
+    status = lib.ppipe_split_points(ctypes.byref(desc), ok)
+    if status != 0:
+        raise _err(lib, status)
+    return list(ok)
+
+
+def prepartition(layer_us: Sequence[float], split_ok: Sequence[int], n_blocks: int) -> List[int]:
+    """Block boundaries [b0 = 0, b1, ..., n_layers] of the pre-partitioning
+    (ppipe_prepartition)."""
+    lib = load_library()
+    n = len(layer_us)
+    t = (ctypes.c_double * n)(*layer_us)
+    ok = (ctypes.c_int32 * (n + 1))(*split_ok)
+    out = (ctypes.c_int32 * (n + 1))()
+    nb = ctypes.c_int32(0)
+    status = lib.ppipe_prepartition(t, ok, n, n_blocks, out, ctypes.byref(nb))
+    if status != 0:
+        raise _err(lib, status)
+    return list(out[:nb.value + 1])
 
 
 class Partition:

@@ -11,8 +11,9 @@ namespace ppipe {
 enum DType : int { DT_F32 = 0, DT_F16 = 1, DT_BF16 = 2 };
 
 // Timing events for the next kernel launch of this host thread (set by the
-// runtime's timed runs, null otherwise).  With events set, launches go
-// through hipExtLaunchKernelGGL, which records them around the kernel itself.
+// runtime's timed runs, null otherwise; either may be null alone).  With an
+// event set, launches go through hipExtLaunchKernelGGL, which records the
+// start event before and the stop event after the kernel itself.
 struct LaunchEvents {
     hipEvent_t start = nullptr, stop = nullptr;
 };
@@ -21,7 +22,7 @@ LaunchEvents& launch_events();
 #define PPIPE_LAUNCH(KERNEL, GRID, BLOCK, SHMEM, STREAM, ...)                                   \
     do {                                                                                         \
         const ::ppipe::LaunchEvents ev_ = ::ppipe::launch_events();                              \
-        if (ev_.start)                                                                           \
+        if (ev_.start || ev_.stop)                                                               \
             hipExtLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, ev_.start, ev_.stop, 0u,   \
                                   __VA_ARGS__);                                                  \
         else                                                                                     \

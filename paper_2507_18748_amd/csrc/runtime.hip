@@ -890,6 +890,43 @@ struct Events {
     }
 };
 
+struct EventPool {
+    std::vector<hipEvent_t> ev;
+    ~EventPool()
+    {
+        for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+    }
+    hipError_t make(int n)
+    {
+        ev.assign(n, nullptr);
+        for (hipEvent_t& e : ev) {
+            const hipError_t r = hipEventCreate(&e);
+            if (r != hipSuccess) return r;
+        }
+        return hipSuccess;
+    }
+};
+
+// Hands layer i's event pair to its first launch (start) and its last launch
+// (stop), so that the pair spans the layer's kernels in a run.
+struct LayerEventsHook : LaunchHook {
+    LayerEventsHook(const std::vector<hipEvent_t>& e, int b) : ev(e), batch(b) {}
+    ~LayerEventsHook() override { launch_events() = LaunchEvents{}; }
+    const std::vector<hipEvent_t>& ev;
+    int batch, layer = 0;
+    void before(const LayerRT& l, int li, hipStream_t) override
+    {
+        const int n = layer_launches(l, batch);
+        launch_events() = LaunchEvents{li == 0 ? ev[2 * layer] : nullptr,
+                                       li == n - 1 ? ev[2 * layer + 1] : nullptr};
+    }
+    void after(const LayerRT& l, int li, hipStream_t) override
+    {
+        launch_events() = LaunchEvents{};
+        if (li == layer_launches(l, batch) - 1) ++layer;
+    }
+};
+
 template <typename F>
 hipError_t time_reps(hipStream_t s, Events& ev, int reps, F&& enqueue, std::vector<float>& us)
 {
@@ -1024,20 +1061,30 @@ int ppipe_profile_layers(ppipe_partition* h, const int32_t* batch_sizes, int32_t
     hipError_t e = ev.make();
     if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipEventCreate", e));
     const int nl = (int)h->L.size();
+    EventPool lev;
+    if ((e = lev.make(2 * nl)) != hipSuccess)
+        return fail(PPIPE_E_HIP, hip_msg("hipEventCreate", e));
     for (int j = 0; j < n_batches; ++j) {
         const int b = batch_sizes[j];
         for (int w = 0; w < warmup && e == hipSuccess; ++w)
             e = enqueue_all(h, b, pb.in, pb.out, pb.s, nullptr);
         if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("kernel launch", e));
-        for (int i = 0; i < nl; ++i) {
-            std::vector<float> t;
-            for (int k = 0; k < PROFILE_TRIALS && e == hipSuccess; ++k)
-                e = time_reps(pb.s, ev, reps, [&] {
-                    return enqueue_layer(h, h->L[i], b, pb.in, pb.out, pb.s, nullptr);
-                }, t);
-            if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("profile run", e));
-            if (out_us) out_us[(size_t)i * n_batches + j] = median_of(t);
+        // in sequence: every repetition runs the range in layer order; layer
+        // i's time runs from its first kernel's start to its last kernel's end
+        std::vector<std::vector<float>> t(nl);
+        for (int r = 0; r < reps && e == hipSuccess; ++r) {
+            LayerEventsHook hook(lev.ev, b);
+            e = enqueue_all(h, b, pb.in, pb.out, pb.s, &hook);
+            if (e == hipSuccess) e = hipStreamSynchronize(pb.s);
+            for (int i = 0; i < nl && e == hipSuccess; ++i) {
+                float ms = 0;
+                e = hipEventElapsedTime(&ms, lev.ev[2 * i], lev.ev[2 * i + 1]);
+                t[i].push_back(ms * 1000.0f);
+            }
         }
+        if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("profile run", e));
+        for (int i = 0; i < nl; ++i)
+            if (out_us) out_us[(size_t)i * n_batches + j] = median_of(t[i]);
         // whole range as run() executes it: one captured graph replayed
         hipGraph_t g = nullptr;
         hipGraphExec_t x = nullptr;
@@ -1048,13 +1095,13 @@ int ppipe_profile_layers(ppipe_partition* h, const int32_t* batch_sizes, int32_t
             if (e == hipSuccess) e = le;
         }
         if (e == hipSuccess) e = hipGraphInstantiate(&x, g, nullptr, nullptr, 0);
-        std::vector<float> t;
+        std::vector<float> tp;
         for (int k = 0; k < PROFILE_TRIALS && e == hipSuccess; ++k)
-            e = time_reps(pb.s, ev, reps, [&] { return hipGraphLaunch(x, pb.s); }, t);
+            e = time_reps(pb.s, ev, reps, [&] { return hipGraphLaunch(x, pb.s); }, tp);
         if (x) (void)hipGraphExecDestroy(x);
         if (g) (void)hipGraphDestroy(g);
         if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("profile graph run", e));
-        if (out_partition_us) out_partition_us[j] = median_of(t);
+        if (out_partition_us) out_partition_us[j] = median_of(tp);
     }
     return PPIPE_OK;
 }
@@ -1163,6 +1210,60 @@ int ppipe_profile_kernels_cold(ppipe_partition* h, int32_t batch, int32_t reps,
             rec.min_us = *std::min_element(t.begin(), t.end());
         }
     }
+    return PPIPE_OK;
+}
+
+int ppipe_split_points(const ppipe_model_desc* desc, int32_t* ok)
+{
+    if (!desc || !desc->layers || desc->n_layers < 1 || !ok)
+        return fail(PPIPE_E_INVALID, "null or empty model description");
+    const int n = desc->n_layers;
+    // earliest layer index read by any layer at or after p (src -1 = model input)
+    int earliest = n;   // sentinel: nothing read
+    for (int p = n; p >= 0; --p) {
+        if (p < n) {
+            const ppipe_layer_desc& ld = desc->layers[p];
+            earliest = std::min(earliest, ld.src);
+            if (ld.res_src >= 0) earliest = std::min(earliest, ld.res_src);
+        }
+        ok[p] = (p == 0 || p == n || earliest >= p - 1) ? 1 : 0;
+    }
+    return PPIPE_OK;
+}
+
+int ppipe_prepartition(const double* layer_us, const int32_t* split_ok, int32_t n_layers,
+                       int32_t n_blocks, int32_t* block_begin, int32_t* n_out)
+{
+    if (!layer_us || !split_ok || !block_begin || !n_out || n_layers < 1 || n_blocks < 1)
+        return fail(PPIPE_E_INVALID, "null argument, no layers or no blocks");
+    double total = 0;
+    for (int i = 0; i < n_layers; ++i) {
+        if (!(layer_us[i] >= 0.0)) return fail(PPIPE_E_INVALID, "negative or NaN layer latency");
+        total += layer_us[i];
+    }
+    const double target = total / n_blocks;
+    int nb = 0, start = 0;
+    while (start < n_layers) {
+        block_begin[nb++] = start;
+        // the valid end whose block latency is closest to the target (the
+        // earliest of equally close ones); sums only grow, so the scan stops
+        // once the sum exceeds the target by the best gap found
+        double sum = 0, best_gap = -1;
+        int best_end = n_layers;
+        for (int p = start + 1; p <= n_layers; ++p) {
+            sum += layer_us[p - 1];
+            if (p < n_layers && !split_ok[p]) continue;
+            const double gap = std::fabs(sum - target);
+            if (best_gap < 0 || gap < best_gap) {
+                best_gap = gap;
+                best_end = p;
+            }
+            if (sum - target >= best_gap) break;
+        }
+        start = best_end;
+    }
+    block_begin[nb] = n_layers;
+    *n_out = nb;
     return PPIPE_OK;
 }
 

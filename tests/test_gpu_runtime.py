@@ -107,3 +107,31 @@ def test_isolated_cold_profile_records_every_launch():
         launches = sum(part.layer_info(i, 8)["kernel_count"] for i in range(wl.begin, wl.end))
         assert len(recs) == launches
         assert all(r["min_us"] > 0 and r["min_us"] <= r["median_us"] for r in recs)
+
+
+def test_chained_blocks_match_the_whole_range_bitwise():
+    """Pre-partitioned blocks run one after another give the same bits as the
+    range run as one partition (every launch plan depends on the layer shape
+    and batch only), and close the range exactly."""
+    import torch
+    from paper_2507_18748_amd import Partition, split_points, prepartition
+    wl, m, P = _small()
+    x = wl.input(8)
+    ok = split_points(m.layers)
+    flops = []
+    with Partition(m.layers, P, (3, 224, 224), wl.begin, wl.end, wl.dtype, max_batch=8) as part:
+        ref = gpu_forward(part, x)
+        flops = [part.layer_info(i, 1)["flops_b1"] + 1e6 for i in range(wl.begin, wl.end)]
+    local_ok = [1] + [ok[p] for p in range(wl.begin + 1, wl.end)] + [1]
+    bounds = [wl.begin + b for b in prepartition(flops, local_ok, 3)]
+    assert bounds[0] == wl.begin and bounds[-1] == wl.end and len(bounds) >= 3
+    cur = upload_nhwc(x, wl.dtype)
+    s = torch.cuda.current_stream().cuda_stream
+    for bb, be in zip(bounds, bounds[1:]):
+        with Partition(m.layers, P, (3, 224, 224), bb, be, wl.dtype, max_batch=8) as bp:
+            out = empty_out(bp, 8)
+            bp.run(8, cur.data_ptr(), out.data_ptr(), s)
+            torch.cuda.synchronize()
+        cur = out
+    got = cur.float().cpu().numpy().transpose(0, 3, 1, 2)
+    np.testing.assert_array_equal(got.reshape(ref.shape), ref)
