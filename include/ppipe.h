@@ -173,6 +173,17 @@ int ppipe_profile_kernels(ppipe_partition* h, int32_t batch, int32_t warmup,
                           int32_t reps, ppipe_kernel_record* records,
                           int32_t capacity, int32_t* count);
 
+/* Partition-boundary quantisation (Implementation section: fp32 feature
+ * maps cross a partition boundary as fp16, halving the transfer).  Converts
+ * n elements of `in` (in_dtype) into `out` (out_dtype) on `stream`,
+ * asynchronously, on the current HIP device.  Narrowing rounds to nearest
+ * even, overflows to +-inf, keeps subnormals and NaN; widening is exact.
+ * in / out: device pointers, caller-owned, not overlapping, NHWC order
+ * unchanged.  Returns a status (PPIPE_E_INVALID for a bad dtype, n < 0 or a
+ * null buffer with n > 0). */
+int ppipe_cast(const void* in, int32_t in_dtype, void* out, int32_t out_dtype, int64_t n,
+               void* stream);
+
 /* ---- pre-partitioning (host only, no device needed) ---- */
 
 /* Valid partition boundaries of a model: ok[p] (p = 0 .. n_layers) is 1 when

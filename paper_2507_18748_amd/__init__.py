@@ -3,7 +3,7 @@ latency table (the data-parallel computation that dominates PPipe's run
 time).  The compute lives in hand-written gfx950 HIP kernels behind the C ABI
 declared in include/ppipe.h; this package is the thin ctypes binding."""
 from .binding import (Partition, PpipeError, load_library, LIB_PATH, OPS, ACTS,
-                      DTYPES, split_points, prepartition)
+                      DTYPES, split_points, prepartition, cast)
 
 __all__ = ["Partition", "PpipeError", "load_library", "LIB_PATH", "OPS", "ACTS", "DTYPES",
-           "split_points", "prepartition"]
+           "split_points", "prepartition", "cast"]

@@ -122,6 +122,8 @@ def load_library() -> ctypes.CDLL:
     lib.ppipe_layer_info.argtypes = [vp, i32, i32, ctypes.POINTER(LayerInfo)]
     lib.ppipe_partition_destroy.restype = None
     lib.ppipe_partition_destroy.argtypes = [vp]
+    lib.ppipe_cast.restype = ctypes.c_int
+    lib.ppipe_cast.argtypes = [vp, i32, vp, i32, ctypes.c_int64, vp]
     lib.ppipe_split_points.restype = ctypes.c_int
     lib.ppipe_split_points.argtypes = [ctypes.POINTER(ModelDesc), ctypes.POINTER(i32)]
     lib.ppipe_prepartition.restype = ctypes.c_int
@@ -141,6 +143,14 @@ def _err(lib, status: int):
 
 def _attr(L, name, default=None):
     return L[name] if isinstance(L, dict) else getattr(L, name, default)
+
+
+def cast(x_ptr: int, in_dtype: str, y_ptr: int, out_dtype: str, n: int, stream: int = 0):
+    """Boundary quantisation: n elements converted on the device (ppipe_cast)."""
+    lib = load_library()
+    status = lib.ppipe_cast(x_ptr, DTYPES[in_dtype], y_ptr, DTYPES[out_dtype], n, stream)
+    if status != 0:
+        raise _err(lib, status)
 
 
 def split_points(layers: Sequence) -> List[int]:

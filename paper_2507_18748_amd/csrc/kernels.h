@@ -148,6 +148,10 @@ const char* maxpool_name(int dt);
 hipError_t launch_gap(int dt, const void* x, void* y, int N, int HW, int C, hipStream_t s);
 const char* gap_name(int dt);
 
+// n elements of x (in_dt) converted to y (out_dt); narrowing rounds to
+// nearest even.
+hipError_t launch_cast(const void* x, int in_dt, void* y, int out_dt, size_t n, hipStream_t s);
+
 // Read `buf` (all but its last 16 MiB, which receive one result per
 // thread): isolated-cold profiling, evicts L2 and the memory-side cache
 // before a timed launch.  bytes >= 32 MiB.

@@ -289,7 +289,57 @@ __global__ void __launch_bounds__(256) sweep_kernel(const uint4* __restrict__ a,
     res[(size_t)blockIdx.x * 256 + threadIdx.x] = acc;
 }
 
+// Element-wise conversion between storage types (partition-boundary
+// quantisation), 4 elements per thread; the last thread takes the tail.
+// Narrowing rounds to nearest even (overflow to +-inf, subnormals kept).
+template <typename Ti, typename To>
+__global__ void __launch_bounds__(256) cast_kernel(const Ti* __restrict__ x, To* __restrict__ y,
+                                                   size_t n)
+{
+    const size_t i = ((size_t)blockIdx.x * 256 + threadIdx.x) * 4;
+    if (i >= n)
+        return;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+        if (i + q < n)
+            y[i + q] = (To)(float)x[i + q];
+}
+
 static unsigned blocks_for(size_t n) { return (unsigned)((n + 255) / 256); }
+
+template <typename Ti>
+static hipError_t launch_cast_to(const void* x, int out_dt, void* y, size_t n, hipStream_t s)
+{
+    const dim3 grid(blocks_for((n + 3) / 4));
+    switch (out_dt) {
+    case DT_F32:
+        PPIPE_LAUNCH((cast_kernel<Ti, float>), grid, dim3(256), 0, s, (const Ti*)x, (float*)y, n);
+        break;
+    case DT_F16:
+        PPIPE_LAUNCH((cast_kernel<Ti, _Float16>), grid, dim3(256), 0, s, (const Ti*)x,
+                     (_Float16*)y, n);
+        break;
+    case DT_BF16:
+        PPIPE_LAUNCH((cast_kernel<Ti, __bf16>), grid, dim3(256), 0, s, (const Ti*)x,
+                     (__bf16*)y, n);
+        break;
+    default:
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_cast(const void* x, int in_dt, void* y, int out_dt, size_t n, hipStream_t s)
+{
+    if (n == 0)
+        return hipSuccess;
+    switch (in_dt) {
+    case DT_F32:  return launch_cast_to<float>(x, out_dt, y, n, s);
+    case DT_F16:  return launch_cast_to<_Float16>(x, out_dt, y, n, s);
+    case DT_BF16: return launch_cast_to<__bf16>(x, out_dt, y, n, s);
+    default:      return hipErrorInvalidValue;
+    }
+}
 
 hipError_t launch_cache_sweep(void* buf, size_t bytes, hipStream_t s)
 {

@@ -1213,6 +1213,19 @@ int ppipe_profile_kernels_cold(ppipe_partition* h, int32_t batch, int32_t reps,
     return PPIPE_OK;
 }
 
+int ppipe_cast(const void* in, int32_t in_dtype, void* out, int32_t out_dtype, int64_t n,
+               void* stream)
+{
+    if (n < 0 || in_dtype < PPIPE_F32 || in_dtype > PPIPE_BF16 || out_dtype < PPIPE_F32 ||
+        out_dtype > PPIPE_BF16)
+        return fail(PPIPE_E_INVALID, "bad dtype or negative element count");
+    if (n > 0 && (!in || !out)) return fail(PPIPE_E_INVALID, "null buffer");
+    const hipError_t e = launch_cast(in, in_dtype, out, out_dtype, (size_t)n,
+                                     (hipStream_t)stream);
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("cast launch", e));
+    return PPIPE_OK;
+}
+
 int ppipe_split_points(const ppipe_model_desc* desc, int32_t* ok)
 {
     if (!desc || !desc->layers || desc->n_layers < 1 || !ok)

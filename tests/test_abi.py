@@ -118,3 +118,11 @@ def test_timing_calls_reject_a_null_handle():
     assert lib.ppipe_partition_run_timed(None, None) == -1
     assert lib.ppipe_timing_read(None, (KernelRecord * 1)(), 1, ctypes.byref(n)) == -1
     assert lib.ppipe_timing_setup(None, 1, None, None) == -1
+
+
+def test_cast_rejects_bad_arguments():
+    from paper_2507_18748_amd.binding import load_library
+    lib = load_library()
+    assert lib.ppipe_cast(None, 0, None, 7, 4, None) == -1      # bad output dtype
+    assert lib.ppipe_cast(None, 0, None, 1, -1, None) == -1     # negative count
+    assert lib.ppipe_cast(None, 0, None, 1, 8, None) == -1      # null buffers
