@@ -270,6 +270,77 @@ def blocks_report(args):
                       "blocks_over_whole": out["blocks_over_whole"]}))
 
 
+def vgpu_report(args):
+    """Latency under virtual GPUs (Sec. 5.3): for k = 1..4 the GPU's compute
+    units are split into k equal shares (CU-masked streams; the paper uses
+    MPS) and the same partition runs on every share side by side, one handle
+    per share, each replaying its captured graph, so the interference
+    between co-located shares is part of the measurement (the paper profiles
+    the same way).  Reports per batch each share's latency and the GPU's
+    aggregate images/s."""
+    import numpy as np
+    import torch
+    import workloads as W
+    from paper_2507_18748_amd import Partition, stream_cu_share, stream_destroy
+    wl = W.workload(args.workload)
+    batches = parse_batches(args.batches)
+    m = wl.build_model()
+    P = wl.params(m)
+    torch.cuda.set_device(0)
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[wl.dtype]
+    x = wl.input(max(batches))
+    xh = torch.from_numpy(np.ascontiguousarray(x.transpose(0, 2, 3, 1))).to(tdt)
+    reps = args.vgpu_reps
+    out = {"workload": wl.name, "layers": [wl.begin, wl.end], "batches": batches,
+           "shares": {}, "method": "k handles on k CU-masked streams (CU i in share (i/8) mod k), "
+                                   "graphs replayed side by side; latency = elapsed / reps per "
+                                   "stream, HIP events on each stream"}
+    for k in (1, 2, 3, 4):
+        parts = [Partition(m.layers, P, (m.in_c, m.in_h, m.in_w), wl.begin, wl.end, wl.dtype,
+                           max_batch=max(batches)) for _ in range(k)]
+        streams = [stream_cu_share(j, k) for j in range(k)]
+        ext = [torch.cuda.ExternalStream(st) for st in streams]
+        info = parts[0].info
+        odt = torch.float32 if info["out_dtype"] == 0 else tdt
+        ins = [xh.cuda() for _ in range(k)]
+        outs = [torch.empty((max(batches), info["out_h"], info["out_w"], info["out_c"]),
+                            dtype=odt, device="cuda") for _ in range(k)]
+        rows = {}
+        for b in batches:
+            for j in range(k):
+                parts[j].capture(b, ins[j].data_ptr(), outs[j].data_ptr())
+            for _ in range(3):
+                for j in range(k):
+                    parts[j].run(b, ins[j].data_ptr(), outs[j].data_ptr(), streams[j])
+            torch.cuda.synchronize()
+            e0 = [torch.cuda.Event(enable_timing=True) for _ in range(k)]
+            e1 = [torch.cuda.Event(enable_timing=True) for _ in range(k)]
+            for j in range(k):
+                e0[j].record(ext[j])
+            for _ in range(reps):
+                for j in range(k):
+                    parts[j].run(b, ins[j].data_ptr(), outs[j].data_ptr(), streams[j])
+            for j in range(k):
+                e1[j].record(ext[j])
+            torch.cuda.synchronize()
+            lat = [e0[j].elapsed_time(e1[j]) * 1e3 / reps for j in range(k)]
+            rows[b] = {"latency_us": lat, "mean_latency_us": float(np.mean(lat)),
+                       "images_per_s": float(sum(b / (t * 1e-6) for t in lat))}
+        out["shares"][k] = rows
+        print(f"[vgpu] {k} share(s) done: b={batches[-1]} mean "
+              f"{rows[batches[-1]]['mean_latency_us']:.1f} us", file=sys.stderr, flush=True)
+        torch.cuda.synchronize()
+        for p_ in parts:
+            p_.close()
+        for st in streams:
+            stream_destroy(st)
+    with open(args.vgpu_out, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps({"vgpu": args.vgpu_out, "workload": wl.name,
+                      "images_per_s_at_max_batch": {k: v[batches[-1]]["images_per_s"]
+                                                    for k, v in out["shares"].items()}}))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -282,6 +353,9 @@ def main():
                     help="pre-partition the workload into --blocks blocks from its latency "
                          "table and write block tables and additivity checks")
     ap.add_argument("--blocks", type=int, default=10, help="N of the pre-partitioning")
+    ap.add_argument("--vgpu-out", default="", metavar="OUT.json",
+                    help="latency of the workload on 1/1, 1/2, 1/3, 1/4 CU shares run side by side")
+    ap.add_argument("--vgpu-reps", type=int, default=20)
     ap.add_argument("--cold-reps", type=int, default=5,
                     help="isolated-cold repetitions per launch (caches swept before each); "
                          "0 skips")
@@ -327,6 +401,8 @@ def main():
         return latency_table(args)
     if args.blocks_out:
         return blocks_report(args)
+    if args.vgpu_out:
+        return vgpu_report(args)
 
     wl = W.workload(args.workload)
     if args.batch:

@@ -184,6 +184,17 @@ int ppipe_profile_kernels(ppipe_partition* h, int32_t batch, int32_t warmup,
 int ppipe_cast(const void* in, int32_t in_dtype, void* out, int32_t out_dtype, int64_t n,
                void* stream);
 
+/* Virtual GPUs (Sec. 5.3: a physical GPU split into 1/1, 1/2, 1/3 or 1/4
+ * shares; the paper uses MPS).  Creates a stream, at default priority, on
+ * the current device whose kernels run only on share `part` of `parts`
+ * near-equal shares of the compute units (CU i of the device's mask
+ * numbering, which goes round-robin over the XCDs, belongs to share
+ * (i / 8) mod parts, so every share keeps CUs on every XCD).  *stream receives a hipStream_t; release it
+ * with ppipe_stream_destroy.  Runs of different handles on the streams of
+ * different shares proceed side by side.  Returns a status. */
+int ppipe_stream_create_cu_share(int32_t part, int32_t parts, void** stream);
+int ppipe_stream_destroy(void* stream);
+
 /* ---- pre-partitioning (host only, no device needed) ---- */
 
 /* Valid partition boundaries of a model: ok[p] (p = 0 .. n_layers) is 1 when

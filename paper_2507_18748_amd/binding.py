@@ -122,6 +122,10 @@ def load_library() -> ctypes.CDLL:
     lib.ppipe_layer_info.argtypes = [vp, i32, i32, ctypes.POINTER(LayerInfo)]
     lib.ppipe_partition_destroy.restype = None
     lib.ppipe_partition_destroy.argtypes = [vp]
+    lib.ppipe_stream_create_cu_share.restype = ctypes.c_int
+    lib.ppipe_stream_create_cu_share.argtypes = [i32, i32, ctypes.POINTER(vp)]
+    lib.ppipe_stream_destroy.restype = ctypes.c_int
+    lib.ppipe_stream_destroy.argtypes = [vp]
     lib.ppipe_cast.restype = ctypes.c_int
     lib.ppipe_cast.argtypes = [vp, i32, vp, i32, ctypes.c_int64, vp]
     lib.ppipe_split_points.restype = ctypes.c_int
@@ -143,6 +147,23 @@ def _err(lib, status: int):
 
 def _attr(L, name, default=None):
     return L[name] if isinstance(L, dict) else getattr(L, name, default)
+
+
+def stream_cu_share(part: int, parts: int) -> int:
+    """hipStream_t (as an int) restricted to share `part` of `parts` of the CUs."""
+    lib = load_library()
+    st = ctypes.c_void_p()
+    status = lib.ppipe_stream_create_cu_share(part, parts, ctypes.byref(st))
+    if status != 0:
+        raise _err(lib, status)
+    return st.value
+
+
+def stream_destroy(stream: int):
+    lib = load_library()
+    status = lib.ppipe_stream_destroy(stream)
+    if status != 0:
+        raise _err(lib, status)
 
 
 def cast(x_ptr: int, in_dtype: str, y_ptr: int, out_dtype: str, n: int, stream: int = 0):

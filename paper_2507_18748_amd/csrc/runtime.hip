@@ -1226,6 +1226,45 @@ int ppipe_cast(const void* in, int32_t in_dtype, void* out, int32_t out_dtype, i
     return PPIPE_OK;
 }
 
+int ppipe_stream_create_cu_share(int32_t part, int32_t parts, void** stream)
+{
+    if (parts < 1 || part < 0 || part >= parts || !stream)
+        return fail(PPIPE_E_INVALID, "need 0 <= part < parts and a stream pointer");
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipGetDevice", e));
+    hipDeviceProp_t prop;
+    if ((e = hipGetDeviceProperties(&prop, dev)) != hipSuccess)
+        return fail(PPIPE_E_HIP, hip_msg("hipGetDeviceProperties", e));
+    const int ncu = prop.multiProcessorCount;
+    if (ncu < parts) return fail(PPIPE_E_INVALID, "more shares than compute units");
+    // CU i belongs to share (i / 8) mod parts.  The mask's CU numbering
+    // goes round-robin over the 8 XCDs, and a mask that leaves an XCD empty
+    // is refused (measured: strides of 2 and 4 fail, every mask below that
+    // keeps CUs on all XCDs works); each share thus spans all XCDs.
+    std::vector<uint32_t> mask((ncu + 31) / 32, 0u);
+    int picked = 0;
+    for (int cu = 0; cu < ncu; ++cu)
+        if ((cu / 8) % parts == part) {
+            mask[cu / 32] |= 1u << (cu % 32);
+            ++picked;
+        }
+    if (picked == 0) return fail(PPIPE_E_INVALID, "empty compute-unit share");
+    hipStream_t st = nullptr;
+    e = hipExtStreamCreateWithCUMask(&st, (uint32_t)mask.size(), mask.data());
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipExtStreamCreateWithCUMask", e));
+    *stream = (void*)st;
+    return PPIPE_OK;
+}
+
+int ppipe_stream_destroy(void* stream)
+{
+    if (!stream) return PPIPE_OK;
+    const hipError_t e = hipStreamDestroy((hipStream_t)stream);
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("hipStreamDestroy", e));
+    return PPIPE_OK;
+}
+
 int ppipe_split_points(const ppipe_model_desc* desc, int32_t* ok)
 {
     if (!desc || !desc->layers || desc->n_layers < 1 || !ok)

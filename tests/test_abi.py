@@ -126,3 +126,13 @@ def test_cast_rejects_bad_arguments():
     assert lib.ppipe_cast(None, 0, None, 7, 4, None) == -1      # bad output dtype
     assert lib.ppipe_cast(None, 0, None, 1, -1, None) == -1     # negative count
     assert lib.ppipe_cast(None, 0, None, 1, 8, None) == -1      # null buffers
+
+
+def test_cu_share_stream_rejects_bad_shares():
+    import ctypes
+    from paper_2507_18748_amd.binding import load_library
+    lib = load_library()
+    st = ctypes.c_void_p()
+    assert lib.ppipe_stream_create_cu_share(2, 2, ctypes.byref(st)) == -1
+    assert lib.ppipe_stream_create_cu_share(0, 0, ctypes.byref(st)) == -1
+    assert lib.ppipe_stream_destroy(None) == 0

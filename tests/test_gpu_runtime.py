@@ -135,3 +135,33 @@ def test_chained_blocks_match_the_whole_range_bitwise():
         cur = out
     got = cur.float().cpu().numpy().transpose(0, 3, 1, 2)
     np.testing.assert_array_equal(got.reshape(ref.shape), ref)
+
+
+@pytest.mark.parametrize("parts", [2, 3])
+def test_runs_on_cu_share_streams_match_the_default_stream(parts):
+    """Virtual GPUs: each share's stream runs its own handle side by side
+    with the others and gives the same bits as a run on the default stream."""
+    import torch
+    from paper_2507_18748_amd import Partition, stream_cu_share, stream_destroy
+    wl, m, P = _small()
+    x = wl.input(4)
+    hs = [Partition(m.layers, P, (3, 224, 224), wl.begin, wl.end, wl.dtype, max_batch=4)
+          for _ in range(parts)]
+    streams = [stream_cu_share(j, parts) for j in range(parts)]
+    try:
+        ref = gpu_forward(hs[0], x)
+        xd = upload_nhwc(x, wl.dtype)
+        outs = [empty_out(h, 4) for h in hs]
+        for _ in range(3):
+            for h, o, st in zip(hs, outs, streams):
+                h.run(4, xd.data_ptr(), o.data_ptr(), st)
+        torch.cuda.synchronize()
+        for o in outs:
+            got = o.float().cpu().numpy().transpose(0, 3, 1, 2)
+            np.testing.assert_array_equal(got.reshape(ref.shape), ref)
+    finally:
+        torch.cuda.synchronize()
+        for st in streams:
+            stream_destroy(st)
+        for h in hs:
+            h.close()
