@@ -1,0 +1,286 @@
+"""Resource-reservation adaptive batching (Sec. 5.4; Alg. 1 and Alg. 2).
+
+The oracle (oracle/batching.py) is pinned to hand-worked cases, brute force
+and invariants.  Host only: no GPU."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import batching as ob
+from workloads import serving as ws
+
+
+def _oracle(gpu_node, pipes):
+    return ob.Cluster(gpu_node), [ob.Pipeline(p["stages"], p["bs"]) for p in pipes]
+
+
+def _lin(a, c, n=8):
+    return [float(a + c * b) for b in range(1, n + 1)]
+
+
+def _single_gpu(bs=4, a=10, c=5):
+    return [0], [{"bs": bs, "stages": [{"gpus": [0], "infer": _lin(a, c), "net": _lin(0, 0)}]}]
+
+
+# ---------------------------------------------------------------- earliest slot
+
+def test_earliest_slot_hand_cases():
+    cl = ob.Cluster([0, 1])
+    g0, g1 = cl.gpu(0), cl.gpu(1)
+    assert cl.earliest_slot([g0], 3.0, 5.0) == 3.0          # nothing reserved
+    cl.mark_reserved(g0, 0.0, 10.0)                          # [0, 10)
+    cl.mark_reserved(g0, 12.0, 8.0)                          # [12, 20)
+    assert cl.earliest_slot([g0], 3.0, 5.0) == 10.0 + 10.0   # gap [10, 12) too short
+    assert cl.earliest_slot([g0], 3.0, 2.0) == 10.0          # fits the gap exactly
+    assert cl.earliest_slot([g0], 20.0, 1.0) == 20.0         # half-open: free at the end
+    assert cl.earliest_slot([g0], 10.0, 0.0) == 10.0         # an instant at a boundary
+    assert cl.earliest_slot([g0], 5.0, 0.0) == 10.0          # an instant inside waits
+    cl.mark_reserved(g1, 8.0, 5.0)                           # [8, 13) on the other one
+    # together: g0 free [10, 12) but g1 busy until 13, then g0 busy until 20
+    assert cl.earliest_slot([g0, g1], 0.0, 1.0) == 20.0
+    assert cl.earliest_slot([g1, g0], 0.0, 1.0) == 20.0
+    cl2 = ob.Cluster([0, 1])
+    cl2.mark_reserved(cl2.gpu(0), 0.0, 4.0)
+    cl2.mark_reserved(cl2.gpu(1), 4.0, 4.0)
+    assert cl2.earliest_slot([cl2.gpu(0), cl2.gpu(1)], 0.0, 1.0) == 8.0
+
+
+def _brute_slot(busy_lists, t, l):
+    """Scan integer start times: with integer interval ends, t and l the
+    earliest slot is an integer."""
+    tau = t
+    while True:
+        if all(not (a < tau + l and tau < b) for busy in busy_lists for (a, b) in busy):
+            return tau
+        tau += 1
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_earliest_slot_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    n_res = int(rng.integers(1, 4))
+    cl = ob.Cluster(list(range(n_res)))
+    lists = []
+    for r in range(n_res):
+        t, busy = 0, []
+        for _ in range(int(rng.integers(0, 6))):
+            t += int(rng.integers(0, 6))
+            d = int(rng.integers(1, 6))
+            busy.append((t, t + d))
+            cl.mark_reserved(cl.gpu(r), float(t), float(d))
+            t += d
+        lists.append(busy)
+    for _ in range(10):
+        t0, l = int(rng.integers(0, 30)), int(rng.integers(1, 8))
+        res = [cl.gpu(r) for r in range(n_res)]
+        assert cl.earliest_slot(res, float(t0), float(l)) == _brute_slot(lists, t0, l)
+
+
+# ---------------------------------------------------------------- probe
+
+def test_probe_figure_example():
+    """The two-pool example of the probing figure: pool 1 holds node 1's GPU,
+    pool 2 the GPUs of nodes 2 and 3; every GPU on its own node.  Node 3's
+    downlink is busy, so node 2 completes first and is chosen; the probe
+    reserves node 1's GPU (t1), node 1's uplink with node 2's downlink at
+    the same time (t2), then node 2's GPU (t3)."""
+    gpu_node = [0, 1, 2]
+    pipe = {"bs": 1, "stages": [{"gpus": [0], "infer": [10.0], "net": [0.0]},
+                                {"gpus": [1, 2], "infer": [20.0], "net": [5.0]}]}
+    cl, (p,) = _oracle(gpu_node, [pipe])
+    cl.mark_reserved(cl.downlink(2), 0.0, 30.0)
+    path, resv, finish, wait = ob.probe(cl, p, 1, 0.0)
+    assert path == [0, 1]
+    assert resv == [(("gpu", 0), 0.0, 10.0), (("ul", 0), 10.0, 5.0), (("dl", 1), 10.0, 5.0),
+                    (("gpu", 1), 15.0, 20.0)]
+    assert finish == 35.0 and wait == 0.0
+    # node 2's GPU busy for long: node 3 wins despite its late downlink
+    cl.mark_reserved(cl.gpu(1), 0.0, 100.0)
+    path, resv, finish, wait = ob.probe(cl, p, 1, 0.0)
+    assert path == [0, 2]
+    assert resv[1:] == [(("ul", 0), 30.0, 5.0), (("dl", 2), 30.0, 5.0), (("gpu", 2), 35.0, 20.0)]
+    assert finish == 55.0 and wait == 20.0
+
+
+def test_probe_shared_node_links():
+    """GPUs of one node share its downlink: a busy downlink delays the
+    transfer to either GPU of that node, and the tie goes to the first."""
+    gpu_node = [0, 1, 1]
+    pipe = {"bs": 1, "stages": [{"gpus": [0], "infer": [1.0], "net": [0.0]},
+                                {"gpus": [1, 2], "infer": [4.0], "net": [3.0]}]}
+    cl, (p,) = _oracle(gpu_node, [pipe])
+    cl.mark_reserved(cl.downlink(1), 1.0, 3.0)   # node 1's downlink, used by both GPUs 1 and 2
+    path, resv, finish, wait = ob.probe(cl, p, 1, 0.0)
+    assert path == [0, 1]
+    assert resv[1] == (("ul", 0), 4.0, 3.0) and resv[2] == (("dl", 1), 4.0, 3.0)
+    assert resv[1][1] == 4.0 and finish == 4.0 + 3.0 + 4.0 and wait == 3.0
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_probe_single_stage_is_optimal(seed):
+    """With one stage the greedy choice is the exact optimum: the minimum
+    over the pool of each GPU's brute-force earliest completion."""
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 5))
+    cl = ob.Cluster(list(range(n)))
+    lists = []
+    for g in range(n):
+        busy, t = [], int(rng.integers(0, 5))
+        for _ in range(int(rng.integers(0, 4))):
+            d = int(rng.integers(1, 9))
+            busy.append((t, t + d))
+            cl.mark_reserved(cl.gpu(g), float(t), float(d))
+            t += d + int(rng.integers(0, 7))
+        lists.append(busy)
+    lat = [float(v) for v in rng.integers(1, 9, size=4)]
+    p = ob.Pipeline([{"gpus": list(range(n)), "infer": lat, "net": [0.0] * 4}], 1)
+    for bs in range(1, 5):
+        now = int(rng.integers(0, 10))
+        best = min(_brute_slot([lists[g]], now, int(lat[bs - 1])) + lat[bs - 1] for g in range(n))
+        assert ob.probe(cl, p, bs, float(now))[2] == best
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_probe_greedy_per_stage(seed):
+    """Every stage's GPU completes that stage no later than any other GPU of
+    its pool would, given the stages before it (Alg. 2's per-pool rule), and
+    the reserved intervals chain: transfer after the previous inference, the
+    two links at the same time, inference after the transfer."""
+    gpu_node, pipes = ws.random_plan(seed, integer=True)
+    cl, ps = _oracle(gpu_node, pipes)
+    rng = np.random.default_rng(seed + 1000)
+    for g in range(len(gpu_node)):                # some random prior load
+        cl.mark_reserved(cl.gpu(g), float(rng.integers(0, 20)), float(rng.integers(1, 30)))
+    for p in ps:
+        bs = p.bs
+        path, resv, finish, _ = ob.probe(cl, p, bs, 5.0)
+        k, t = 0, 5.0
+        for si, st in enumerate(p.stages):
+            prev_end = t
+            if si > 0:
+                (u, tu, lu), (d, td, ld) = resv[k], resv[k + 1]
+                assert tu == td and tu >= t and lu == ld == st["net"][bs - 1]
+                assert u == cl.uplink(path[si - 1]) and d == cl.downlink(path[si])
+                t, k = tu + lu, k + 2
+            (gres, tg, lg) = resv[k]
+            assert gres == cl.gpu(path[si]) and tg >= t and lg == st["infer"][bs - 1]
+            stage_end = tg + lg
+            for alt in st["gpus"]:                 # no other GPU of the pool finishes earlier
+                ta = prev_end
+                if si > 0:
+                    links = [cl.uplink(path[si - 1]), cl.downlink(alt)]
+                    ta = cl.earliest_slot(links, prev_end, st["net"][bs - 1]) + st["net"][bs - 1]
+                e = cl.earliest_slot([cl.gpu(alt)], ta, st["infer"][bs - 1]) + st["infer"][bs - 1]
+                assert stage_end <= e
+            t, k = stage_end, k + 1
+        assert finish == t
+
+
+# ---------------------------------------------------------------- Alg. 1 decisions
+
+def test_wait_then_deadline_dispatch():
+    """One GPU, inference 10 + 5 b, unified batch 4, SLO 100: a lone
+    request at 0 fits a batch of 4 but only 1 is queued, so the scheduler
+    waits until 100 - 15 = 85 and then sends the batch of 1, finishing
+    exactly at the deadline."""
+    gpu_node, pipes = _single_gpu()
+    cl, ps = _oracle(gpu_node, pipes)
+    q = [{"id": 0, "arrival": 0.0, "deadline": 100.0}]
+    d = ob.decide(cl, ps, q, 0.0)
+    assert d["kind"] == "wait" and d["bs"] == 4 and d["wake"] == 85.0
+    d = ob.decide(cl, ps, q, 85.0, deadline_wake=True)
+    assert d["kind"] == "dispatch" and d["bs"] == 1 and d["start"] == 85.0 and d["finish"] == 100.0
+    assert ob.decide(cl, ps, q, 85.0)["kind"] == "idle"
+    log = ob.simulate(*_oracle(gpu_node, pipes), [0.0], 100.0)
+    assert [x["kind"] for x in log] == ["wait", "dispatch"] and log[1]["now"] == 85.0
+
+
+def test_drop_when_even_one_misses():
+    gpu_node, pipes = _single_gpu()
+    cl, ps = _oracle(gpu_node, pipes)
+    q = [{"id": 7, "arrival": 0.0, "deadline": 14.0}]      # batch 1 takes 15
+    d = ob.decide(cl, ps, q, 0.0)
+    assert d["kind"] == "drop" and d["id"] == 7 and q == []
+
+
+def test_full_batch_dispatches_at_once():
+    gpu_node, pipes = _single_gpu()
+    log = ob.simulate(*_oracle(gpu_node, pipes), [0.0, 1.0, 2.0, 3.0], 100.0)
+    assert [x["kind"] for x in log] == ["wait", "wait", "wait", "dispatch"]
+    assert [x["wake"] for x in log[:3]] == [85.0, 80.0, 75.0]  # slack shrinks as the queue grows
+    assert log[3]["bs"] == 4 and log[3]["finish"] == 3.0 + 30.0 and log[3]["ids"] == [0, 1, 2, 3]
+
+
+def test_batch_shrinks_to_meet_deadline_then_drop():
+    """SLO 27: batch 4 (30) is too slow, batch 3 (25) fits; four requests
+    at time 0.  The first three wait, then leave as a batch of 3 (the chosen
+    bs* is 3, not the unified 4); the fourth then finds the GPU busy until
+    25 and cannot finish by 27 at any size, so it is dropped."""
+    gpu_node, pipes = _single_gpu()
+    log = ob.simulate(*_oracle(gpu_node, pipes), [0.0] * 4, 27.0)
+    kinds = [(x["kind"], x.get("bs")) for x in log]
+    assert kinds == [("wait", 3), ("wait", 3), ("dispatch", 3), ("drop", None)]
+    assert log[0]["wake"] == 12.0 and log[1]["wake"] == 7.0
+    assert log[2]["finish"] == 25.0 and log[3]["id"] == 3
+
+
+def test_pipeline_choice_by_wait():
+    """Two single-GPU pipelines; the first one's GPU is busy until 50, so the
+    second waits less and gets the batch; a pipeline with no wait but a slow
+    path still wins on the waiting-time rule."""
+    gpu_node = [0, 1]
+    pipes = [{"bs": 1, "stages": [{"gpus": [0], "infer": _lin(10, 0), "net": _lin(0, 0)}]},
+             {"bs": 1, "stages": [{"gpus": [1], "infer": _lin(40, 0), "net": _lin(0, 0)}]}]
+    cl, ps = _oracle(gpu_node, pipes)
+    cl.mark_reserved(cl.gpu(0), 0.0, 50.0)
+    q = [{"id": 0, "arrival": 0.0, "deadline": 1000.0}]
+    d = ob.decide(cl, ps, q, 0.0)
+    assert d["kind"] == "dispatch" and d["pipeline"] == 1 and d["finish"] == 40.0
+    # no load anywhere: equal (zero) waits, the first pipeline wins the tie
+    cl, ps = _oracle(gpu_node, pipes)
+    q = [{"id": 0, "arrival": 0.0, "deadline": 1000.0}]
+    assert ob.decide(cl, ps, q, 0.0)["pipeline"] == 0
+
+
+def test_drop_restarts_from_pipeline_choice():
+    """After a drop the next request is decided afresh (a new round of
+    Alg. 1): the first request is hopeless, the second is served."""
+    gpu_node, pipes = _single_gpu(bs=1)
+    cl, ps = _oracle(gpu_node, pipes)
+    q = [{"id": 0, "arrival": 0.0, "deadline": 5.0}, {"id": 1, "arrival": 0.0, "deadline": 50.0}]
+    assert ob.decide(cl, ps, q, 0.0)["kind"] == "drop"
+    d = ob.decide(cl, ps, q, 0.0)
+    assert d["kind"] == "dispatch" and d["id"] == 1
+
+
+def _check_log(log, arrivals, slo, cl):
+    """Invariants of a finished simulation: every request dispatched or
+    dropped exactly once; a dispatch meets every member's deadline, starts
+    no earlier than its decision and takes the oldest queued requests; the
+    reservation tables never overlap."""
+    seen = []
+    for d in log:
+        if d["kind"] == "dispatch":
+            assert d["start"] >= d["now"]
+            for i in d["ids"]:
+                assert d["finish"] <= arrivals[i] + slo
+            seen += d["ids"]
+        elif d["kind"] == "drop":
+            seen.append(d["id"])
+    assert sorted(seen) == list(range(len(arrivals)))
+    assert seen == sorted(seen)                    # queue order: oldest first
+    assert ob.reserved_overlaps(cl) == 0
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_oracle_invariants_random(seed):
+    gpu_node, pipes = ws.random_plan(seed, integer=seed % 2 == 0)
+    cap = ws.plan_capacity_per_us(pipes)
+    arr = ws.poisson_arrivals(cap * (0.5 + 0.15 * (seed % 6)), 300, seed)
+    slo = 4 * max(sum(s["infer"][p["bs"] - 1] + s["net"][p["bs"] - 1] for s in p["stages"])
+                  for p in pipes)
+    cl, ps = _oracle(gpu_node, pipes)
+    log = ob.simulate(cl, ps, list(arr), slo)
+    _check_log(log, arr, slo, cl)
+    assert any(d["kind"] == "dispatch" for d in log)

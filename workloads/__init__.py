@@ -2,7 +2,8 @@
 
 This package holds only *inputs*: CNN architectures written as fused-layer
 lists, and seeded generators for weights, batch-norm statistics and input
-images.  It contains none of the forward-pass arithmetic (no convolution,
+images, plus seeded request traces and cluster plans for the request
+scheduler (serving.py).  It contains none of the forward-pass arithmetic (no convolution,
 pooling, normalisation folding or shape inference); both the CPU oracle and
 the GPU library consume what it produces, and neither imports the other.
 """
