@@ -270,6 +270,120 @@ def blocks_report(args):
                       "blocks_over_whole": out["blocks_over_whole"]}))
 
 
+def serving_plan(table, out_bytes, bounds, batches, n_nodes=12, per_node=8, bs=8,
+                 link_gbps=400.0, link_fixed_us=5.0):
+    """A pooled-pipeline plan over a measured layer table for the request
+    scheduler: three pipelines sharing n_nodes x per_node GPUs, cut at
+    pre-partitioning block boundaries, pools sized to their stage's latency
+    at the unified batch size `bs`.
+      P0: two stages cut at the boundary nearest half the model's latency,
+      P1: three stages cut nearest the thirds,
+      P2: the whole model on one pool (no partitioning).
+    Stage latency at batch b is the sum of its layers' latencies (partition
+    latency adds up, Sec. 5.1); the transfer into a stage moves the previous
+    layer's output, out_bytes[j - 1] * b bytes, over a node link of
+    link_gbps plus a fixed link_fixed_us."""
+    import numpy as np
+    n_gpus = n_nodes * per_node
+    jb = batches.index(bs)
+    cum = np.concatenate([[0.0], np.cumsum(table[:, jb])])
+    total = cum[-1]
+
+    def cut(frac):
+        return min(bounds[1:-1], key=lambda b: abs(cum[b] - frac * total))
+
+    shapes = [[0, cut(0.5), len(table)],
+              [0, cut(1 / 3), cut(2 / 3), len(table)],
+              [0, len(table)]]
+    shares = [32, 36, 28]
+    gpu_node = [g // per_node for g in range(n_gpus)]
+    nxt, pipes = 0, []
+    for sh, share in zip(shapes, shares):
+        lat = [float(cum[e] - cum[b]) for b, e in zip(sh, sh[1:])]
+        pools = [max(1, int(round(share * v / sum(lat)))) for v in lat]
+        pools[-1] = share - sum(pools[:-1])
+        stages = []
+        for (b, e), k in zip(zip(sh, sh[1:]), pools):
+            infer = [float(table[b:e, j].sum()) for j in range(len(batches))]
+            moved = out_bytes[b - 1] if b > 0 else 0
+            net = [link_fixed_us + moved * bb / (link_gbps / 8 * 1e3) for bb in batches]
+            stages.append({"gpus": list(range(nxt, nxt + k)), "infer": infer, "net": net,
+                           "layers": [b, e]})
+            nxt += k
+        pipes.append({"bs": bs, "stages": stages})
+    return gpu_node, pipes
+
+
+def batching_report(args):
+    """Resource-reservation adaptive batching (Sec. 5.4) fed by the measured
+    per-layer table: the layer table of the workload is measured at every
+    batch 1..B, cut into pre-partitioning blocks, turned into a 96-GPU
+    pooled-pipeline plan, and the native scheduler then serves seeded
+    Poisson and bursty request streams at several loads.  Reports drops,
+    deadline misses (must be 0), reservation overlaps (must be 0) and the
+    host cost of a decision."""
+    import numpy as np
+    import torch
+    import workloads as W
+    from workloads import serving as ws
+    from paper_2507_18748_amd import Partition, Batcher, split_points, prepartition
+    wl = W.workload(args.workload)
+    batches = parse_batches(args.batches)
+    if batches != list(range(1, batches[-1] + 1)):
+        raise SystemExit("--batching needs every batch 1..B (e.g. --batches 1-16)")
+    m = wl.build_model()
+    P = wl.params(m)
+    torch.cuda.set_device(0)
+    in_chw = (m.in_c, m.in_h, m.in_w)
+    with Partition(m.layers, P, in_chw, wl.begin, wl.end, wl.dtype,
+                   max_batch=max(batches)) as part:
+        table, whole = part.profile_layers(batches, warmup=3, reps=args.profile_reps)
+        out_bytes = [part.layer_info(i, 1)["out_bytes_b1"] for i in range(wl.begin, wl.end)]
+    print("[batching] layer table done", file=sys.stderr, flush=True)
+    ok = split_points(m.layers)
+    local_ok = [1] + [ok[p] for p in range(wl.begin + 1, wl.end)] + [1]
+    bs = min(8, batches[-1])
+    bounds = prepartition([float(v) for v in table[:, batches.index(bs)]], local_ok, args.blocks)
+    gpu_node, pipes = serving_plan(table, out_bytes, bounds, batches, bs=bs)
+    cap = ws.plan_capacity_per_us(pipes)
+    path_us = max(sum(s["infer"][bs - 1] + s["net"][bs - 1] for s in p["stages"]) for p in pipes)
+    slo = 2.0 * path_us
+    runs = []
+    for kind in ("poisson", "bursty"):
+        for load in (0.5, 0.8, 0.95):
+            gen = ws.poisson_arrivals if kind == "poisson" else ws.bursty_arrivals
+            arr = gen(cap * load, args.requests, 17)
+            with Batcher(gpu_node, pipes) as b:
+                st, _ = b.simulate(arr, slo)
+                overlaps, held = b.check()
+            nb = max(st["batches"], 1)
+            runs.append({"arrivals": kind, "load": load, "requests": st["requests"],
+                         "dropped_frac": st["dropped"] / st["requests"], "late": st["late"],
+                         "overlaps": overlaps, "reservations": held,
+                         "mean_batch": st["dispatched"] / nb,
+                         "dispatch_probes": st["dispatch_probes"] / nb,
+                         "dispatch_us": st["dispatch_us"] / nb,
+                         "probes_per_batch_all": st["probes"] / nb,
+                         "us_per_batch_all": st["decision_us"] / nb,
+                         "served_per_s": st["dispatched"] / (arr[-1] * 1e-6)})
+            print(f"[batching] {kind} load {load}: {runs[-1]}", file=sys.stderr, flush=True)
+    plan = [{"bs": p["bs"], "stages": [{"layers": s["layers"], "gpus": len(s["gpus"]),
+                                        f"infer_us_b{bs}": s["infer"][bs - 1],
+                                        f"net_us_b{bs}": s["net"][bs - 1]} for s in p["stages"]]}
+            for p in pipes]
+    out = {"workload": wl.name, "batches": batches, "blocks": [wl.begin + b for b in bounds],
+           "gpus": len(gpu_node), "nodes": max(gpu_node) + 1, "plan": plan,
+           "capacity_per_s": cap * 1e6, "slo_us": slo, "runs": runs,
+           "arrivals": "seeded synthetic (Poisson; bursty = Poisson bursts of geometric size)"}
+    with open(args.batching_out, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps({"batching": args.batching_out, "slo_us": slo,
+                      "capacity_per_s": out["capacity_per_s"],
+                      "runs": [{k: r[k] for k in ("arrivals", "load", "dropped_frac", "late",
+                                                  "overlaps", "dispatch_probes", "dispatch_us")}
+                               for r in runs]}))
+
+
 def vgpu_report(args):
     """Latency under virtual GPUs (Sec. 5.3): for k = 1..4 the GPU's compute
     units are split into k equal shares (CU-masked streams; the paper uses
@@ -356,6 +470,10 @@ def main():
     ap.add_argument("--vgpu-out", default="", metavar="OUT.json",
                     help="latency of the workload on 1/1, 1/2, 1/3, 1/4 CU shares run side by side")
     ap.add_argument("--vgpu-reps", type=int, default=20)
+    ap.add_argument("--batching-out", default="", metavar="OUT.json",
+                    help="serve synthetic request streams with the adaptive batching "
+                         "scheduler over the workload's measured table (--batches 1-B)")
+    ap.add_argument("--requests", type=int, default=200000)
     ap.add_argument("--cold-reps", type=int, default=5,
                     help="isolated-cold repetitions per launch (caches swept before each); "
                          "0 skips")
@@ -403,6 +521,8 @@ def main():
         return blocks_report(args)
     if args.vgpu_out:
         return vgpu_report(args)
+    if args.batching_out:
+        return batching_report(args)
 
     wl = W.workload(args.workload)
     if args.batch:

@@ -216,6 +216,114 @@ int ppipe_split_points(const ppipe_model_desc* desc, int32_t* ok);
 int ppipe_prepartition(const double* layer_us, const int32_t* split_ok, int32_t n_layers,
                        int32_t n_blocks, int32_t* block_begin, int32_t* n_out);
 
+/* ---- resource-reservation adaptive batching (host only, no device) ----
+ *
+ * The request scheduler of Sec. 5.4 (Alg. 1 and Alg. 2 of the appendix).
+ * A cluster has GPUs on nodes; each node has one uplink and one downlink
+ * shared by its GPUs.  A pooled pipeline is a chain of stages (partitions);
+ * each stage is a pool of GPUs that all hold that partition.  The scheduler
+ * keeps, for every GPU, uplink and downlink, the time intervals reserved on
+ * it, and for each decision
+ *  1. probes every pipeline at its unified batch size and takes the one
+ *     whose path waits least for its resources (sum over the path's
+ *     transfers and inferences of slot start - earliest possible start);
+ *  2. probes that pipeline from its unified batch size down to 1 and takes
+ *     the first size whose completion meets the oldest queued request's
+ *     deadline;
+ *  3. drops the oldest request if no size does; waits if fewer requests are
+ *     queued than that size (until the queued requests would just still
+ *     meet the oldest deadline); otherwise reserves the probed intervals
+ *     and dispatches that many requests from the head of the queue.
+ * A probe walks the stages in order and, in each pool, takes the GPU that
+ * completes the stage earliest (first such GPU in pool order): the transfer
+ * into a stage needs the previous GPU's uplink and this GPU's downlink free
+ * together for the transfer latency, then this GPU free for the inference
+ * latency, each at the earliest such time (earliest slot).  Two slips of the
+ * printed pseudocode are read as the prose states them: the drop test is on
+ * the chosen batch size, and what is reserved is the chosen batch's probe.
+ * Times are microseconds on any common clock.  A handle is not thread-safe.
+ */
+#define PPIPE_MAX_STAGES 16
+
+typedef struct {
+    int32_t n_stages;              /* 1 .. PPIPE_MAX_STAGES */
+    const int32_t* stage_n_gpus;   /* [n_stages], each >= 1 */
+    const int32_t* stage_gpus;     /* GPU ids of stage 0's pool, then stage 1's, ... */
+    int32_t max_bs;                /* latency tables cover batch 1 .. max_bs */
+    int32_t unified_bs;            /* the plan's batch size for this pipeline, <= max_bs */
+    const double* infer_us;        /* [n_stages][max_bs]: stage s at batch b -> [s][b-1] */
+    const double* net_us;          /* [n_stages][max_bs]: transfer into stage s (row 0 unused) */
+} ppipe_pipeline_desc;
+
+typedef enum {
+    PPIPE_DECISION_IDLE = 0,       /* queue empty */
+    PPIPE_DECISION_DISPATCH = 1,   /* bs requests from first_id on leave on `path` */
+    PPIPE_DECISION_DROP = 2,       /* request first_id cannot meet its deadline */
+    PPIPE_DECISION_WAIT = 3        /* call again at wake_us or at the next arrival */
+} ppipe_decision_kind;
+
+typedef struct {
+    int32_t kind;                  /* ppipe_decision_kind */
+    int32_t pipeline;              /* chosen pipeline (-1 when idle) */
+    int32_t bs;                    /* dispatched / awaited batch size; 1 for a drop */
+    int32_t probes;                /* probes this decision made */
+    int64_t first_id;              /* id of the first dispatched or the dropped request */
+    double start_us;               /* dispatch: first stage's inference start */
+    double finish_us;              /* dispatch: last stage's inference end */
+    double deadline_us;            /* dispatch: the oldest dispatched request's deadline */
+    double wake_us;                /* wait: when the queued requests must go (else +inf) */
+    int32_t path[PPIPE_MAX_STAGES];/* dispatch: GPU of each stage */
+} ppipe_decision;
+
+typedef struct {
+    int64_t requests, dispatched, dropped;
+    int64_t late;                  /* dispatched requests finishing after their deadline */
+    int64_t batches, decisions, probes;
+    int64_t dispatch_probes;       /* probes made by the decisions that dispatched */
+    double decision_us;            /* host wall time of every decision */
+    double dispatch_us;            /* host wall time of the decisions that dispatched */
+    double max_finish_us;
+} ppipe_sim_stats;
+
+typedef struct ppipe_batcher ppipe_batcher;
+
+/* Builds a scheduler over n_gpus GPUs; gpu_node[g] is GPU g's node (NULL:
+ * one node per GPU).  Copies every table; the caller keeps its arrays.
+ * Returns NULL on a bad description (status PPIPE_E_INVALID). */
+ppipe_batcher* ppipe_batcher_create(int32_t n_gpus, const int32_t* gpu_node,
+                                    int32_t n_pipelines, const ppipe_pipeline_desc* pipelines);
+void ppipe_batcher_destroy(ppipe_batcher* b);
+
+/* Queues a request; arrivals must be non-decreasing.  Returns a status. */
+int ppipe_batcher_submit(ppipe_batcher* b, int64_t id, double arrival_us, double deadline_us);
+
+/* One decision at time now_us.  deadline_wake != 0 marks a call at the
+ * wake_us of a previous WAIT: the queued requests go now, so the batch size
+ * is capped at the queue length.  A DISPATCH or DROP changes the state;
+ * call again until IDLE or WAIT.  Returns a status. */
+int ppipe_batcher_step(ppipe_batcher* b, double now_us, int32_t deadline_wake,
+                       ppipe_decision* d);
+
+/* Probe without reserving: completion time, waiting time and path (n_stages
+ * entries, may be NULL) of a batch of bs (1 .. max_bs) on `pipeline` at
+ * now_us.  Returns a status. */
+int ppipe_batcher_probe(ppipe_batcher* b, int32_t pipeline, int32_t bs, double now_us,
+                        double* finish_us, double* wait_us, int32_t* path);
+
+/* Invariant check: *overlaps = pairs of overlapping reservations on any
+ * resource (0 for a correct scheduler), *intervals = reservations held. */
+int ppipe_batcher_check(const ppipe_batcher* b, int64_t* overlaps, int64_t* intervals);
+
+/* Event-driven run over n requests arriving at arrivals_us (sorted), each
+ * with deadline arrival + slo_us and id = its index: a decision round at
+ * every arrival (steps until IDLE or WAIT) and at every pending wake-up.
+ * Continues on the handle's state.  Fills *stats; writes up to
+ * log_capacity non-idle decisions to log (may be NULL) and their number to
+ * *log_count (may be NULL).  Returns a status. */
+int ppipe_batcher_simulate(ppipe_batcher* b, const double* arrivals_us, int64_t n,
+                           double slo_us, ppipe_sim_stats* stats, ppipe_decision* log,
+                           int64_t log_capacity, int64_t* log_count);
+
 /* Isolated-cold per-launch timing at one batch: before each of `reps`
  * repetitions of a launch, a sweep reads `sweep_bytes` of a private buffer
  * (>= 32 MiB; 512 MiB or more evicts L2 and the 256 MB memory-side cache), so

@@ -18,6 +18,7 @@ ACTS = {"none": 0, "relu": 1, "relu6": 2}
 DTYPES = {"f32": 0, "f16": 1, "bf16": 2}
 
 _fp = ctypes.POINTER(ctypes.c_float)
+_dp = ctypes.POINTER(ctypes.c_double)
 
 
 class LayerDesc(ctypes.Structure):
@@ -66,6 +67,36 @@ class KernelRecord(ctypes.Structure):
 
 
 STATUS = {0: "OK", -1: "INVALID", -2: "SPLIT", -3: "UNSUPPORTED", -4: "NOMEM", -5: "HIP"}
+
+
+MAX_STAGES = 16
+DECISIONS = {0: "idle", 1: "dispatch", 2: "drop", 3: "wait"}
+
+
+class PipelineDesc(ctypes.Structure):
+    _fields_ = [("n_stages", ctypes.c_int32),
+                ("stage_n_gpus", ctypes.POINTER(ctypes.c_int32)),
+                ("stage_gpus", ctypes.POINTER(ctypes.c_int32)),
+                ("max_bs", ctypes.c_int32),
+                ("unified_bs", ctypes.c_int32),
+                ("infer_us", ctypes.POINTER(ctypes.c_double)),
+                ("net_us", ctypes.POINTER(ctypes.c_double))]
+
+
+class Decision(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("pipeline", ctypes.c_int32),
+                ("bs", ctypes.c_int32), ("probes", ctypes.c_int32),
+                ("first_id", ctypes.c_int64),
+                ("start_us", ctypes.c_double), ("finish_us", ctypes.c_double),
+                ("deadline_us", ctypes.c_double), ("wake_us", ctypes.c_double),
+                ("path", ctypes.c_int32 * MAX_STAGES)]
+
+
+class SimStats(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in ("requests", "dispatched", "dropped", "late",
+                                              "batches", "decisions", "probes",
+                                              "dispatch_probes")] + \
+               [(n, ctypes.c_double) for n in ("decision_us", "dispatch_us", "max_finish_us")]
 
 
 class PpipeError(RuntimeError):
@@ -133,6 +164,22 @@ def load_library() -> ctypes.CDLL:
     lib.ppipe_prepartition.restype = ctypes.c_int
     lib.ppipe_prepartition.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i32), i32,
                                        i32, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+    lib.ppipe_batcher_create.restype = vp
+    lib.ppipe_batcher_create.argtypes = [i32, ctypes.POINTER(i32), i32, ctypes.POINTER(PipelineDesc)]
+    lib.ppipe_batcher_destroy.restype = None
+    lib.ppipe_batcher_destroy.argtypes = [vp]
+    lib.ppipe_batcher_submit.restype = ctypes.c_int
+    lib.ppipe_batcher_submit.argtypes = [vp, ctypes.c_int64, ctypes.c_double, ctypes.c_double]
+    lib.ppipe_batcher_step.restype = ctypes.c_int
+    lib.ppipe_batcher_step.argtypes = [vp, ctypes.c_double, i32, ctypes.POINTER(Decision)]
+    lib.ppipe_batcher_probe.restype = ctypes.c_int
+    lib.ppipe_batcher_probe.argtypes = [vp, i32, i32, ctypes.c_double, _dp, _dp, ctypes.POINTER(i32)]
+    lib.ppipe_batcher_check.restype = ctypes.c_int
+    lib.ppipe_batcher_check.argtypes = [vp, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int64)]
+    lib.ppipe_batcher_simulate.restype = ctypes.c_int
+    lib.ppipe_batcher_simulate.argtypes = [vp, _dp, ctypes.c_int64, ctypes.c_double,
+                                           ctypes.POINTER(SimStats), ctypes.POINTER(Decision),
+                                           ctypes.c_int64, ctypes.POINTER(ctypes.c_int64)]
     lib.ppipe_last_error.restype = ctypes.c_char_p
     lib.ppipe_last_error.argtypes = []
     lib.ppipe_last_status.restype = ctypes.c_int32
@@ -204,6 +251,112 @@ def prepartition(layer_us: Sequence[float], split_ok: Sequence[int], n_blocks: i
     if status != 0:
         raise _err(lib, status)
     return list(out[:nb.value + 1])
+
+
+def _decision(d: Decision, n_stages: int = MAX_STAGES) -> dict:
+    out = {"kind": DECISIONS[d.kind], "pipeline": d.pipeline, "bs": d.bs, "probes": d.probes}
+    if d.kind == 1:
+        out.update(id=d.first_id, start=d.start_us, finish=d.finish_us, deadline=d.deadline_us,
+                   path=[g for g in d.path[:n_stages] if g >= 0])
+    elif d.kind == 2:
+        out["id"] = d.first_id
+    elif d.kind == 3:
+        out["wake"] = d.wake_us
+    return out
+
+
+class Batcher:
+    """Resource-reservation adaptive batching scheduler (ppipe_batcher_*,
+    Sec. 5.4).
+
+    gpu_node: node of each GPU (GPUs of a node share its uplink/downlink).
+    pipelines: list of {"stages": [{"gpus": [...], "infer": [l(1)..l(B)],
+      "net": [l(1)..l(B)]}, ...], "bs": unified batch size}; every stage of a
+      pipeline has tables of the same length B (net of stage 0 is unused).
+    """
+
+    def __init__(self, gpu_node: Sequence[int], pipelines: Sequence[dict]):
+        self._lib = load_library()
+        self._h = None
+        keep = []
+        descs = (PipelineDesc * len(pipelines))()
+        for d, p in zip(descs, pipelines):
+            st = p["stages"]
+            nb = len(st[0]["infer"])
+            if any(len(x["infer"]) != nb or len(x["net"]) != nb for x in st):
+                raise PpipeError(-1, "stage tables of one pipeline must have equal length")
+            n_g = np.array([len(x["gpus"]) for x in st], np.int32)
+            gp = np.array([g for x in st for g in x["gpus"]], np.int32)
+            inf = np.ascontiguousarray([x["infer"] for x in st], np.float64)
+            net = np.ascontiguousarray([x["net"] for x in st], np.float64)
+            keep += [n_g, gp, inf, net]
+            d.n_stages, d.max_bs, d.unified_bs = len(st), nb, int(p["bs"])
+            d.stage_n_gpus = n_g.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+            d.stage_gpus = gp.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+            d.infer_us = inf.ctypes.data_as(_dp)
+            d.net_us = net.ctypes.data_as(_dp)
+        nodes = (ctypes.c_int32 * len(gpu_node))(*gpu_node)
+        h = self._lib.ppipe_batcher_create(len(gpu_node), nodes, len(pipelines), descs)
+        if not h:
+            raise _err(self._lib, self._lib.ppipe_last_status())
+        self._h = h
+        self._stages = [len(p["stages"]) for p in pipelines]
+
+    def _check(self, status):
+        if status != 0:
+            raise _err(self._lib, status)
+
+    def submit(self, rid: int, arrival: float, deadline: float):
+        self._check(self._lib.ppipe_batcher_submit(self._h, rid, arrival, deadline))
+
+    def step(self, now: float, deadline_wake: bool = False) -> dict:
+        d = Decision()
+        self._check(self._lib.ppipe_batcher_step(self._h, now, int(deadline_wake), ctypes.byref(d)))
+        return _decision(d)
+
+    def probe(self, pipeline: int, bs: int, now: float):
+        """(finish, wait, path) of a probe that reserves nothing."""
+        f, w = ctypes.c_double(), ctypes.c_double()
+        path = (ctypes.c_int32 * MAX_STAGES)()
+        self._check(self._lib.ppipe_batcher_probe(self._h, pipeline, bs, now, ctypes.byref(f),
+                                                  ctypes.byref(w), path))
+        return f.value, w.value, list(path[:self._stages[pipeline]])
+
+    def check(self):
+        """(overlapping reservation pairs, reservations held)."""
+        o, n = ctypes.c_int64(), ctypes.c_int64()
+        self._check(self._lib.ppipe_batcher_check(self._h, ctypes.byref(o), ctypes.byref(n)))
+        return o.value, n.value
+
+    def simulate(self, arrivals: Sequence[float], slo: float, log_capacity: int = 0):
+        """Native event loop (ppipe_batcher_simulate); returns (stats dict,
+        list of decisions)."""
+        arr = np.ascontiguousarray(arrivals, np.float64)
+        st = SimStats()
+        log = (Decision * max(log_capacity, 1))()
+        cnt = ctypes.c_int64()
+        self._check(self._lib.ppipe_batcher_simulate(
+            self._h, arr.ctypes.data_as(_dp), len(arr), slo, ctypes.byref(st),
+            log if log_capacity > 0 else None, log_capacity, ctypes.byref(cnt)))
+        stats = {n: getattr(st, n) for n, _ in SimStats._fields_}
+        return stats, [_decision(log[i]) for i in range(cnt.value)]
+
+    def close(self):
+        if self._h:
+            self._lib.ppipe_batcher_destroy(self._h)
+            self._h = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 class Partition:

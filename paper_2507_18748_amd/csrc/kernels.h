@@ -5,6 +5,7 @@
 #include <hip/hip_ext.h>
 #include <cstddef>
 #include <cstdint>
+#include <string>
 
 namespace ppipe {
 
@@ -29,6 +30,9 @@ LaunchEvents& launch_events();
             hipLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, __VA_ARGS__);                 \
     } while (0)
 enum Act : int { ACT_NONE = 0, ACT_RELU = 1, ACT_RELU6 = 2 };
+
+// Records a failing call's status and message for ppipe_last_error(); returns status.
+int set_error(int status, const std::string& msg);
 
 inline int dtype_size(int dt) { return dt == DT_F32 ? 4 : 2; }
 

@@ -37,6 +37,13 @@ int fail(int code, const std::string& msg)
     return code;
 }
 
+}  // namespace
+
+// the host-only parts of the library report errors through the same slot
+int ppipe::set_error(int status, const std::string& msg) { return fail(status, msg); }
+
+namespace {
+
 std::string hip_msg(const char* what, hipError_t e)
 {
     return std::string(what) + ": " + hipGetErrorString(e);

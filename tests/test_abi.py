@@ -23,7 +23,8 @@ def test_header_declares_the_entry_points():
     names = declared_functions()
     for must in ("ppipe_partition_create", "ppipe_partition_run", "ppipe_profile_layers",
                  "ppipe_partition_info", "ppipe_layer_info", "ppipe_partition_destroy",
-                 "ppipe_last_error", "ppipe_profile_kernels", "ppipe_partition_capture"):
+                 "ppipe_last_error", "ppipe_profile_kernels", "ppipe_partition_capture",
+                 "ppipe_batcher_create", "ppipe_batcher_step", "ppipe_batcher_simulate"):
         assert must in names
     text = open(HEADER).read()
     assert "torch" not in text.lower().replace("pytorch", "") or "at::" not in text

@@ -1,7 +1,9 @@
 """Resource-reservation adaptive batching (Sec. 5.4; Alg. 1 and Alg. 2).
 
 The oracle (oracle/batching.py) is pinned to hand-worked cases, brute force
-and invariants.  Host only: no GPU."""
+and invariants first; the native scheduler behind the C ABI must then make
+exactly the oracle's decisions on seeded random clusters and traces.  All
+host-only: no GPU."""
 import math
 
 import numpy as np
@@ -284,3 +286,195 @@ def test_oracle_invariants_random(seed):
     log = ob.simulate(cl, ps, list(arr), slo)
     _check_log(log, arr, slo, cl)
     assert any(d["kind"] == "dispatch" for d in log)
+
+
+# ---------------------------------------------------------------- library vs oracle
+
+def _lib():
+    from paper_2507_18748_amd import Batcher
+    return Batcher
+
+
+def _same_decision(lib_d, ora_d):
+    assert lib_d["kind"] == ora_d["kind"]
+    if lib_d["kind"] == "idle":
+        return
+    assert lib_d["pipeline"] == ora_d["pipeline"]
+    if lib_d["kind"] == "dispatch":
+        for k in ("bs", "id", "path", "start", "finish", "deadline"):
+            assert lib_d[k] == ora_d[k], k
+    elif lib_d["kind"] == "drop":
+        assert lib_d["id"] == ora_d["id"]
+    else:
+        assert lib_d["bs"] == ora_d["bs"] and lib_d["wake"] == ora_d["wake"]
+
+
+def test_library_hand_cases():
+    B = _lib()
+    gpu_node, pipes = _single_gpu()
+    with B(gpu_node, pipes) as b:
+        _, log = b.simulate([0.0] * 4, 27.0, log_capacity=16)
+        assert [(d["kind"], d["bs"]) for d in log] == [("wait", 3), ("wait", 3), ("dispatch", 3),
+                                                       ("drop", 1)]
+        assert log[0]["wake"] == 12.0 and log[2]["finish"] == 25.0 and log[3]["id"] == 3
+    gpu_node = [0, 1, 2]
+    pipe = {"bs": 1, "stages": [{"gpus": [0], "infer": [10.0], "net": [0.0]},
+                                {"gpus": [1, 2], "infer": [20.0], "net": [5.0]}]}
+    with B(gpu_node, [pipe]) as b:
+        assert b.probe(0, 1, 0.0) == (35.0, 0.0, [0, 1])
+        b.submit(0, 0.0, 100.0)
+        d = b.step(0.0)
+        assert d["kind"] == "dispatch" and d["path"] == [0, 1] and d["finish"] == 35.0
+        assert b.step(0.0)["kind"] == "idle"
+        # after the reservation the second pool's other GPU completes first
+        assert b.probe(0, 1, 0.0) == (45.0, 10.0, [0, 2])
+        assert b.check() == (0, 4)
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_library_matches_oracle_simulation(seed):
+    B = _lib()
+    gpu_node, pipes = ws.random_plan(seed, integer=seed % 3 == 0)
+    cap = ws.plan_capacity_per_us(pipes)
+    load = 0.4 + 0.2 * (seed % 5)
+    n = 250
+    arr = (ws.bursty_arrivals if seed % 4 == 3 else ws.poisson_arrivals)(cap * load, n, seed)
+    slo = (2 + seed % 4) * max(sum(s["infer"][p["bs"] - 1] + s["net"][p["bs"] - 1]
+                                   for s in p["stages"]) for p in pipes)
+    cl, ps = _oracle(gpu_node, pipes)
+    ora = ob.simulate(cl, ps, list(arr), slo)
+    with B(gpu_node, pipes) as b:
+        stats, lib = b.simulate(arr, slo, log_capacity=4 * n)
+        assert b.check()[0] == 0
+        assert b.check()[1] == sum(len(v) for v in cl.table.values())
+    assert len(lib) == len(ora)
+    for x, y in zip(lib, ora):
+        _same_decision(x, y)
+    assert stats["requests"] == n and stats["late"] == 0
+    assert stats["dispatched"] + stats["dropped"] == n
+    assert stats["batches"] == sum(d["kind"] == "dispatch" for d in ora)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_library_step_api_matches_oracle(seed):
+    """Driving the scheduler call by call (submit, step) gives the oracle's
+    decisions too, including the capped decision at a wake-up."""
+    B = _lib()
+    gpu_node, pipes = ws.random_plan(100 + seed)
+    cap = ws.plan_capacity_per_us(pipes)
+    arr = ws.poisson_arrivals(cap * 0.9, 120, seed)
+    slo = 3 * max(sum(s["infer"][p["bs"] - 1] + s["net"][p["bs"] - 1] for s in p["stages"])
+                  for p in pipes)
+    cl, ps = _oracle(gpu_node, pipes)
+    q = []
+    with B(gpu_node, pipes) as b:
+        nxt, wake = 0, math.inf
+        while nxt < len(arr) or q:
+            if nxt < len(arr) and arr[nxt] <= wake:
+                now, forced = float(arr[nxt]), False
+                q.append({"id": nxt, "arrival": now, "deadline": now + slo})
+                b.submit(nxt, now, now + slo)
+                nxt += 1
+            else:
+                now, forced = wake, True
+            wake = math.inf
+            while True:
+                x = b.step(now, forced)
+                y = ob.decide(cl, ps, q, now, forced)
+                forced = False
+                _same_decision(x, y)
+                if y["kind"] == "idle":
+                    break
+                if y["kind"] == "wait":
+                    wake = y["wake"]
+                    break
+
+
+def test_library_rejects_bad_input():
+    from paper_2507_18748_amd import PpipeError
+    B = _lib()
+    ok = {"bs": 2, "stages": [{"gpus": [0], "infer": _lin(1, 1, 4), "net": _lin(0, 0, 4)}]}
+    bad = [
+        ([0], [{**ok, "bs": 5}]),                                                   # bs > max_bs
+        ([0], [{**ok, "stages": [{**ok["stages"][0], "gpus": [1]}]}]),             # GPU id
+        ([0], [{**ok, "stages": [{**ok["stages"][0], "gpus": []}]}]),              # empty pool
+        ([0], [{**ok, "stages": [{**ok["stages"][0], "infer": [-1.0] * 4}]}]),     # negative
+        ([0], [{**ok, "stages": [{**ok["stages"][0], "net": [math.nan] * 4}]}]),   # NaN
+        ([-1], [ok]),                                                              # node id
+        ([0], []),                                                                 # no pipeline
+    ]
+    for gpu_node, pipes in bad:
+        with pytest.raises(PpipeError):
+            B(gpu_node, pipes)
+    with B([0], [ok]) as b:
+        b.submit(0, 5.0, 10.0)
+        with pytest.raises(PpipeError):
+            b.submit(1, 4.0, 10.0)                 # out of arrival order
+        for args in [(1, 1, 0.0), (0, 0, 0.0), (0, 5, 0.0), (0, 1, math.inf)]:
+            with pytest.raises(PpipeError):
+                b.probe(*args)
+        with pytest.raises(PpipeError):
+            b.simulate([2.0, 1.0], 10.0)           # unsorted
+        with pytest.raises(PpipeError):
+            b.simulate([6.0], 0.0)                 # SLO must be positive
+
+
+def test_library_dispatch_cost():
+    """Cost of a decision at cluster scale: 96 GPUs (12 nodes of 8) in three
+    pooled pipelines, Poisson load at 0.8 of the plan's capacity.  Reports
+    probes and host microseconds per dispatched batch; the bound asserted
+    here is loose (a slow shared CI host), the measured figure is printed."""
+    B = _lib()
+    gpu_node = ws.node_layout(12, 8)
+    rng = np.random.default_rng(5)
+    tab = ws.random_tables(rng, 3, 16, integer=False)
+    g = iter(range(96))
+    pipes = [{"bs": 8, "stages": [{"gpus": [next(g) for _ in range(16)], "infer": tab["infer"][i],
+                                   "net": tab["net"][i]} for i in range(2)]} for _ in range(2)]
+    pipes.append({"bs": 8, "stages": [{"gpus": [next(g) for _ in range(32)],
+                                       "infer": [a + b for a, b in zip(tab["infer"][0],
+                                                                       tab["infer"][1])],
+                                       "net": tab["net"][2]}]})
+    cap = ws.plan_capacity_per_us(pipes)
+    arr = ws.poisson_arrivals(cap * 0.8, 200000, 5)
+    slo = 5 * (pipes[0]["stages"][0]["infer"][7] + pipes[0]["stages"][1]["infer"][7])
+    with B(gpu_node, pipes) as b:
+        stats, _ = b.simulate(arr, slo)
+        assert b.check()[0] == 0
+    assert stats["late"] == 0 and stats["batches"] > 0
+    nb = stats["batches"]
+    us = stats["dispatch_us"] / nb
+    print(f"\n{nb} batches; dispatching decision: {stats['dispatch_probes'] / nb:.2f} probes, "
+          f"{us:.2f} us; all decisions per batch: {stats['probes'] / nb:.2f} probes, "
+          f"{stats['decision_us'] / nb:.2f} us; dropped {stats['dropped'] / stats['requests']:.4f}")
+    assert us < 100.0
+
+
+def test_bench_serving_plan_shape():
+    """The plan the benchmark builds from a layer table: 96 GPUs dealt out
+    once each, every pipeline's stages tile the model at block boundaries,
+    stage latencies are the sums of their layers' rows, transfers carry the
+    previous layer's output."""
+    import bench
+    rng = np.random.default_rng(3)
+    n, batches = 40, list(range(1, 9))
+    table = np.outer(rng.uniform(1, 9, n), batches)
+    out_bytes = [int(v) for v in rng.integers(1000, 9000, n)]
+    bounds = [0, 7, 13, 22, 30, 40]
+    gpu_node, pipes = bench.serving_plan(table, out_bytes, bounds, batches, bs=8)
+    assert len(gpu_node) == 96 and gpu_node[8] == 1
+    used = sorted(g for p in pipes for s in p["stages"] for g in s["gpus"])
+    assert used == list(range(96))
+    assert [len(p["stages"]) for p in pipes] == [2, 3, 1]
+    for p in pipes:
+        edges = [s["layers"][0] for s in p["stages"]] + [p["stages"][-1]["layers"][1]]
+        assert edges[0] == 0 and edges[-1] == n and set(edges) <= set(bounds)
+        for s in p["stages"]:
+            b, e = s["layers"]
+            assert s["infer"][7] == pytest.approx(table[b:e, 7].sum())
+            if b > 0:
+                assert s["net"][0] == pytest.approx(5.0 + out_bytes[b - 1] / 50e3)
+    with _lib()(gpu_node, pipes) as sched:
+        st, _ = sched.simulate(ws.poisson_arrivals(ws.plan_capacity_per_us(pipes) * 0.8, 5000, 1),
+                               3 * max(sum(s["infer"][7] for s in p["stages"]) for p in pipes))
+        assert st["late"] == 0 and sched.check()[0] == 0
