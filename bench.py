@@ -98,12 +98,13 @@ def cold_summary(records, dtype):
 
 
 def source_digest():
-    """sha256 over the kernel and runtime sources (any change invalidates
-    HBM counters taken before it)."""
+    """sha256 over the kernel and runtime sources, the HIP files and their
+    shared header (any change invalidates HBM counters taken before it; the
+    host-only request scheduler is not part of it)."""
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2507_18748_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    for f in sorted(x for x in os.listdir(csrc) if x.endswith((".hip", ".h"))):
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + b"\0" + fh.read())
     return h.hexdigest()
