@@ -9,7 +9,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libppipe.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
-SOURCES = ["conv_gemm.hip", "mem_kernels.hip", "runtime.hip", "batcher.cpp"]
+SOURCES = ["conv_gemm.hip", "pointwise.hip", "mem_kernels.hip", "runtime.hip", "batcher.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",

@@ -1008,6 +1008,7 @@ GemmCfgInfo gemm_cfg_info(int cfg)
     case GEMM_DMA_64x64_S2: return {64, 64, 8, false, 2, 4};
     case GEMM_DMA_64x64_S3: return {64, 64, 8, false, 3, 4};
     case GEMM_DMA_128x128_8W_S2: return {128, 128, 8, false, 2, 8};
+    case GEMM_PW:       return {16, 16, 4, false, 0, 4};
     case GEMM_DMA_128x128_8W_S3: return {128, 128, 8, false, 3, 8};
     case GEMM_DMA_64x64_8W_S2: return {64, 64, 8, false, 2, 8};
     case GEMM_DMA_64x64_8W_S3: return {64, 64, 8, false, 3, 8};
@@ -1107,6 +1108,8 @@ static hipError_t launch_cfg(int cfg, int wk, bool tapv, const ConvGemmArgs& a,
 hipError_t launch_conv_gemm(int dt, int cfg, int wk, bool tapv, const ConvGemmArgs& a,
                             hipStream_t s)
 {
+    if (cfg == GEMM_PW)
+        return tapv ? hipErrorInvalidValue : launch_pointwise(dt, wk, a, a.grid_blocks, s);
     switch (dt) {
     case DT_F32:  return launch_cfg<float>(cfg, wk, tapv, a, s);
     case DT_F16:  return launch_cfg<_Float16>(cfg, wk, tapv, a, s);
@@ -1170,10 +1173,12 @@ const char* conv_gemm_name(int dt, int cfg, int wk, bool tapv)
 {
     static char names[3][GEMM_NCFG][SKINNY_MAX_WAVES + 1][2][64];
     const GemmCfgInfo c = gemm_cfg_info(cfg);
-    const int w = c.skinny ? wk : 0;
+    const int w = c.skinny || cfg == GEMM_PW ? wk : 0;
     char* n = names[dt][cfg][w][tapv ? 1 : 0];
     if (!n[0]) {
-        if (c.skinny)
+        if (cfg == GEMM_PW)
+            snprintf(n, 64, "pw_conv<%s,cf%d>", dt_name(dt), wk);
+        else if (c.skinny)
             snprintf(n, 64, "conv_gemm_skinny<%s,%dx%d,waves%d>", dt_name(dt), c.bm, c.bn, wk);
         else if (c.dma)
             snprintf(n, 64, "conv_gemm<%s,%dx%d,kv%d%s,dma%d%s>", dt_name(dt), c.bm, c.bn, c.kv,

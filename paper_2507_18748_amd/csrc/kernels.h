@@ -64,6 +64,7 @@ struct ConvGemmArgs {
     int tiles_m, tiles_co;
     int co_fastest;       // tile order: 0 = m tiles of one weight slice adjacent, 1 = co tiles adjacent
     int softmax;          // 1: write fp32 logits for a following softmax
+    int grid_blocks;      // pointwise kernel: cap on blocks along the pixels (0: resident set)
 };
 
 // Tile configurations (rows = co, columns = m).
@@ -89,7 +90,11 @@ enum GemmCfg : int {
     GEMM_DMA_64x64_8W_S3 = 14,    // 8 waves, 3 stages, software-pipelined
     GEMM_DMA_64x64_8W_S4 = 15,    // 8 waves, 4 stages (two in flight)
     GEMM_DMA_64x64_8W_S6 = 16,    // 8 waves, 6 stages (four in flight; few blocks per CU)
-    GEMM_NCFG = 17
+    // Streaming 1x1 convolution (stride 1, C <= 32): weights in registers,
+    // 16-pixel groups loaded straight into MFMA fragments.  wk = 16-channel
+    // fragments per block (pointwise_channel_frags).
+    GEMM_PW = 17,
+    GEMM_NCFG = 18
 };
 struct GemmCfgInfo {
     int bm, bn, kv;       // tile rows (co), columns (m); kv: 16-byte vectors of K per LDS stage
@@ -116,6 +121,13 @@ constexpr int SKINNY_MAX_WAVES = 16;
 hipError_t launch_conv_gemm(int dt, int cfg, int wk, bool tapv, const ConvGemmArgs& a,
                             hipStream_t s);
 const char* conv_gemm_name(int dt, int cfg, int wk, bool tapv);
+
+// Streaming 1x1 convolution (GEMM_PW) of a 16-bit layer with C <= 32 (a
+// multiple of 8), Co % 4 == 0, stride 1, no padding, no K split, no softmax;
+// cf 16-channel fragments per block, at most grid_blocks blocks along the
+// pixels (0: one resident set), each wave walking 16-pixel groups grid-stride.
+hipError_t launch_pointwise(int dt, int cf, const ConvGemmArgs& a, int grid_blocks, hipStream_t s);
+int pointwise_channel_frags(int Co);
 
 // Copy NHWC [npix][C] into [npix][Cp] (Cp > C) with zero channels appended,
 // so that a layer with fewer channels than a 16-byte vector can be gathered

@@ -96,6 +96,7 @@ enum { BUF_IN = -1, BUF_OUT = -2, BUF_NONE = -3 };
 
 struct Plan {
     int cfg, wk, splits, chunks_per_split, total_chunks, tiles_m, tiles_co, co_fastest;
+    int grid = 0;   // pointwise kernel: cap on blocks along the pixels (0: resident set)
 };
 
 struct Shape {
@@ -109,6 +110,7 @@ struct LayerRT {
     int H, W, C, Ho, Wo, Co;
     int kind;
     bool tapv = false, softmax = false, skinny_ok = false, pad_in = false;
+    bool pw_ok = false;         // the streaming 1x1 kernel applies (GEMM_PW)
     int KH = 1, KW = 1, gstride = 1, gpad = 0, K = 0, Kpad = 0;
     int cpad = 0;               // channels as the GEMM reads them (C rounded up to a vector)
     size_t w_off = 0, scale_off = 0, bias_off = 0;
@@ -167,7 +169,7 @@ namespace {
 // shape, waves per tile (skinny) and tile order.  Deterministic in (M, Co, K,
 // dtype, eligibility) so that the latency table, the benchmark and the
 // parity tests exercise the same launches.
-Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok)
+Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok)
 {
     auto tiles = [&](int cfg) {
         GemmCfgInfo c = gemm_cfg_info(cfg);
@@ -219,6 +221,15 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok)
         if (t * splits < 512)
             cfg = GEMM_DMA_64x64_8W_S4;
     }
+    //  * 16-bit 1x1 stride-1 layers with at most 32 input channels and at
+    //    least 16384 output pixels stream through the pointwise kernel (2-3x
+    //    faster on MobileNetV2's large expansion layers; the GEMM stays ahead
+    //    on small grids).  PPIPE_GEMM_NO_PW turns it off for A/B timing.
+    if (pw_ok && M >= 16384 && !std::getenv("PPIPE_GEMM_NO_PW")) {
+        cfg = GEMM_PW;
+        wk = pointwise_channel_frags(Co);
+        splits = 1;
+    }
     // PPIPE_GEMM_PLAN="cfg,waves,splits" forces one configuration on every
     // eligible GEMM layer (tuning sweeps and kernel tests).
     if (const char* env = std::getenv("PPIPE_GEMM_PLAN")) {
@@ -226,7 +237,13 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok)
         if (std::sscanf(env, "%d,%d,%d", &fc, &fw, &fs) >= 1 && fc >= 0 && fc < GEMM_NCFG) {
             const bool sk = gemm_cfg_info(fc).skinny;
             const bool wk_ok = fw == 4 || fw == 8 || (fw == 16 && fc == GEMM_SK_16x16);
-            if (!sk) {
+            if (fc == GEMM_PW) {
+                if (pw_ok) {
+                    cfg = fc;
+                    wk = pointwise_channel_frags(Co);
+                    splits = 1;
+                }
+            } else if (!sk) {
                 cfg = fc;
                 wk = 0;
                 splits = std::max(1, std::min(fs, 64));
@@ -246,6 +263,11 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok)
     p.splits = (p.total_chunks + p.chunks_per_split - 1) / p.chunks_per_split;
     p.tiles_m = (M + c.bn - 1) / c.bn;
     p.tiles_co = (Co + c.bm - 1) / c.bm;
+    if (cfg == GEMM_PW) {   // 16-pixel groups x output-channel slices of wk fragments
+        p.tiles_co = (Co + 16 * wk - 1) / (16 * wk);
+        if (const char* env = std::getenv("PPIPE_PW_GRID"))   // tuning sweeps
+            p.grid = std::max(0, std::atoi(env));
+    }
     p.co_fastest = M > Co ? 1 : 0;   // keep the larger operand's slices on one XCD
     return p;
 }
@@ -393,6 +415,7 @@ hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, 
         a.tiles_co = p.tiles_co;
         a.co_fastest = p.co_fastest;
         a.softmax = l.softmax ? 1 : 0;
+        a.grid_blocks = p.grid;
         if (want(li)) {
             if (hook) hook->before(l, li, s);
             e = launch_conv_gemm(P->dtype, p.cfg, p.wk, tapv_of(l, p), a, s);
@@ -647,6 +670,9 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
             l.tapv = !(l.KH * l.KW == 1 || l.cpad % bk == 0);
             // skinny kernel: each 64-byte K step lies in one (kh, kw) tap
             l.skinny_ok = l.KH * l.KW == 1 || l.cpad % (4 * epv) == 0;
+            // streaming 1x1 kernel: 16-bit, stride 1, unpadded, one MFMA k-step
+            l.pw_ok = dt != DT_F32 && ld.op == PPIPE_OP_CONV && l.KH * l.KW == 1 &&
+                      l.gstride == 1 && l.gpad == 0 && !l.pad_in && x.c <= 32;
             if (l.tapv && l.Kpad / epv > GEMM_VTAB_MAX)
                 return fail(PPIPE_E_UNSUPPORTED, who + ": reduction length " +
                                                      std::to_string(l.K) + " with C = " +
@@ -789,7 +815,7 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
         l.plans.resize(P->max_batch);
         for (int b = 1; b <= P->max_batch; ++b) {
             const int M = b * l.Ho * l.Wo;
-            const Plan p = choose_plan(M, l.Co, l.K, dt, l.skinny_ok);
+            const Plan p = choose_plan(M, l.Co, l.K, dt, l.skinny_ok, l.pw_ok);
             l.plans[b - 1] = p;
             size_t need = 0;
             if (p.splits > 1) need += (size_t)p.splits * M * l.Co;

@@ -52,6 +52,56 @@ def conv(name, src, ci, co, k=1, s=1, p=0, g=1, act="relu", res=-1, bn=True, bia
                 groups=g, act=act, res_src=res, bn=bn, bias=bias)
 
 
+# Streaming 1x1 kernel, forced on small layers: (C, Co, H, W, batch,
+# residual, activation).  Ragged channel slices (Co not a multiple of the
+# slice), C below one k-step, ragged 16-pixel groups.
+PW_CASES = [
+    (8, 4, 5, 7, 3, False, "relu"),
+    (16, 96, 9, 11, 4, False, "relu6"),
+    (24, 144, 7, 7, 5, False, "relu6"),
+    (32, 16, 13, 5, 2, False, "none"),
+    (32, 192, 6, 6, 3, True, "relu"),
+    (24, 36, 5, 5, 2, True, "none"),
+    (16, 200, 4, 4, 1, False, "relu"),
+    (32, 388, 3, 9, 3, False, "relu"),
+]
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("ci,co,h,w,batch,res,act", PW_CASES)
+def test_pointwise_kernel(monkeypatch, dtype, ci, co, h, w, batch, res, act):
+    from paper_2507_18748_amd import Partition
+    monkeypatch.setenv("PPIPE_GEMM_PLAN", "17")
+    if res:   # residual source: a 3x3 convolution of the same input
+        specs = [conv("r", -1, ci, co, 3, 1, 1), conv("c", -1, ci, co, act=act, res=0)]
+    else:
+        specs = [conv("c", -1, ci, co, act=act)]
+    m = make((ci, h, w), specs)
+    with Partition(m.layers, W.model_params(m, 0, dtype), (ci, h, w), 0, len(specs), dtype,
+                   max_batch=batch) as part:
+        assert part.layer_info(len(specs) - 1, batch)["kernel"].startswith("pw_conv<")
+    check(m, dtype, batch)
+
+
+@pytest.mark.parametrize("grid", ["1", "8"])
+def test_pointwise_grid_stride_matches_default(monkeypatch, grid):
+    """A pointwise launch capped at 1 or 8 blocks (every wave walks many
+    16-pixel groups with loads in flight ahead) gives the default's bits."""
+    from paper_2507_18748_amd import Partition
+    m = make((24, 37, 29), [conv("c", -1, 24, 144, act="relu6")])
+    P = W.model_params(m, 0, "bf16")
+    x = W.partition_input((24, 37, 29), 3, 5, "bf16", "normal")
+    outs = []
+    monkeypatch.setenv("PPIPE_GEMM_PLAN", "17")
+    for g in (None, grid):
+        if g:
+            monkeypatch.setenv("PPIPE_PW_GRID", g)
+        with Partition(m.layers, P, (24, 37, 29), 0, 1, "bf16", max_batch=3) as part:
+            assert part.layer_info(0, 3)["kernel"].startswith("pw_conv<")
+            outs.append(gpu_forward(part, x))
+    np.testing.assert_array_equal(outs[0], outs[1])
+
+
 @pytest.mark.parametrize("dtype", DTYPES)
 def test_conv3x3_split_k(dtype):
     # M = 2*15*15 = 450 (ragged), Co = 128: 64x64 tiles with split-K
