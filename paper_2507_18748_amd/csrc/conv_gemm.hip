@@ -1009,6 +1009,7 @@ GemmCfgInfo gemm_cfg_info(int cfg)
     case GEMM_DMA_64x64_S3: return {64, 64, 8, false, 3, 4};
     case GEMM_DMA_128x128_8W_S2: return {128, 128, 8, false, 2, 8};
     case GEMM_PW:       return {16, 16, 4, false, 0, 4};
+    case GEMM_STEM:     return {16, 16, 4, false, 0, 4};
     case GEMM_DMA_128x128_8W_S3: return {128, 128, 8, false, 3, 8};
     case GEMM_DMA_64x64_8W_S2: return {64, 64, 8, false, 2, 8};
     case GEMM_DMA_64x64_8W_S3: return {64, 64, 8, false, 3, 8};
@@ -1110,6 +1111,8 @@ hipError_t launch_conv_gemm(int dt, int cfg, int wk, bool tapv, const ConvGemmAr
 {
     if (cfg == GEMM_PW)
         return tapv ? hipErrorInvalidValue : launch_pointwise(dt, wk, a, a.grid_blocks, s);
+    if (cfg == GEMM_STEM)
+        return tapv ? hipErrorInvalidValue : launch_stem(dt, wk, a, a.grid_blocks, s);
     switch (dt) {
     case DT_F32:  return launch_cfg<float>(cfg, wk, tapv, a, s);
     case DT_F16:  return launch_cfg<_Float16>(cfg, wk, tapv, a, s);
@@ -1173,11 +1176,13 @@ const char* conv_gemm_name(int dt, int cfg, int wk, bool tapv)
 {
     static char names[3][GEMM_NCFG][SKINNY_MAX_WAVES + 1][2][64];
     const GemmCfgInfo c = gemm_cfg_info(cfg);
-    const int w = c.skinny || cfg == GEMM_PW ? wk : 0;
+    const int w = c.skinny || cfg == GEMM_PW || cfg == GEMM_STEM ? wk : 0;
     char* n = names[dt][cfg][w][tapv ? 1 : 0];
     if (!n[0]) {
         if (cfg == GEMM_PW)
             snprintf(n, 64, "pw_conv<%s,cf%d>", dt_name(dt), wk);
+        else if (cfg == GEMM_STEM)
+            snprintf(n, 64, "stem_conv<%s,cf%d>", dt_name(dt), wk);
         else if (c.skinny)
             snprintf(n, 64, "conv_gemm_skinny<%s,%dx%d,waves%d>", dt_name(dt), c.bm, c.bn, wk);
         else if (c.dma)

@@ -94,7 +94,11 @@ enum GemmCfg : int {
     // 16-pixel groups loaded straight into MFMA fragments.  wk = 16-channel
     // fragments per block (pointwise_channel_frags).
     GEMM_PW = 17,
-    GEMM_NCFG = 18
+    // Stem of a C <= 4 channel image: one tap per 16-byte operand vector,
+    // channels gathered per lane, weights staged in LDS.  wk = 16-channel
+    // fragments per block (stem_channel_frags).
+    GEMM_STEM = 18,
+    GEMM_NCFG = 19
 };
 struct GemmCfgInfo {
     int bm, bn, kv;       // tile rows (co), columns (m); kv: 16-byte vectors of K per LDS stage
@@ -128,6 +132,12 @@ const char* conv_gemm_name(int dt, int cfg, int wk, bool tapv);
 // pixels (0: one resident set), each wave walking 16-pixel groups grid-stride.
 hipError_t launch_pointwise(int dt, int cf, const ConvGemmArgs& a, int grid_blocks, hipStream_t s);
 int pointwise_channel_frags(int Co);
+
+// Stem (GEMM_STEM): x is the unpadded image [N][H][W][C], C <= 4 and below
+// one 16-byte vector, weights packed with the channels padded to a vector
+// per tap, at most 52 taps; cf 16-channel fragments per block.
+hipError_t launch_stem(int dt, int cf, const ConvGemmArgs& a, int grid_blocks, hipStream_t s);
+int stem_channel_frags(int Co);
 
 // Copy NHWC [npix][C] into [npix][Cp] (Cp > C) with zero channels appended,
 // so that a layer with fewer channels than a 16-byte vector can be gathered

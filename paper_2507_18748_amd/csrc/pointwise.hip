@@ -1,5 +1,7 @@
-// Streaming 1x1 convolution for layers with few input channels.
+// Streaming convolutions for thin layers: 1x1 layers with few input
+// channels, and stems with a 3-channel input.
 //
+// Pointwise (GEMM_PW).
 // A 1x1, stride-1 convolution with C <= 32 input channels reduces over one
 // 32-element MFMA k-step per output, so the GEMM's machinery (K loop, LDS
 // stage ring, staged epilogue) is overhead: these layers (the expansion and
@@ -17,6 +19,15 @@
 //   * the epilogue (folded BN scale and shift from LDS, residual, activation,
 //     rounding) stores those four channels as one 8-byte vector, so a wave's
 //     store covers 32 contiguous bytes of each of its 16 pixel rows.
+//
+// Stem (GEMM_STEM).  A k x k convolution of a C <= 4 channel image (RGB
+// stems) is bound by writing its output.  The weights are packed as for the
+// GEMM, one 16-byte vector per tap with the channels zero-padded, so a
+// 16-byte MFMA operand vector is one tap: in k-step ks, lane group q handles
+// tap 4 ks + q, gathering the C channels of the input pixel under that tap
+// for its output pixel (zero outside the image) and reading the tap's weight
+// vector from LDS, where the block stages its channel slice once.  The same
+// epilogue follows; fp32 stems run on the 16x16x4 fp32 MFMA.
 #include "kernels.h"
 
 #include <algorithm>
@@ -45,6 +56,16 @@ template <> __device__ __forceinline__ floatx4 pw_mfma<__bf16>(uint4 a, uint4 b,
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
+// fp32: a 16-byte vector is 4 consecutive k; instruction t takes component t
+// of both operands from every lane group, which pairs them as a dot product.
+template <> __device__ __forceinline__ floatx4 pw_mfma<float>(uint4 a, uint4 b, floatx4 c)
+{
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+    return c;
+}
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t pw_rsrc(const void* p, uint32_t bytes)
 {
@@ -61,6 +82,41 @@ __device__ __forceinline__ float pw_act(float v, int act)
     if (act == ACT_RELU) return fmaxf(v, 0.0f);
     if (act == ACT_RELU6) return fminf(fmaxf(v, 0.0f), 6.0f);
     return v;
+}
+
+// Epilogue of four consecutive output channels co.. (c.. within the block's
+// slice) of pixel p: folded BN, residual, activation, one vector store.
+template <typename T>
+__device__ __forceinline__ void pw_store4(const ConvGemmArgs& a, int p, int co, int c,
+                                          const floatx4& acc, const float* s_scale,
+                                          const float* s_bias)
+{
+    const size_t off = (size_t)p * a.Co + co;
+    float v[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) v[r] = acc[r] * s_scale[c + r] + s_bias[c + r];
+    if constexpr (sizeof(T) == 4) {
+        if (a.res) {
+            const float4 u = *(const float4*)((const float*)a.res + off);
+            v[0] += u.x; v[1] += u.y; v[2] += u.z; v[3] += u.w;
+        }
+        *(float4*)((float*)a.y + off) = make_float4(pw_act(v[0], a.act), pw_act(v[1], a.act),
+                                                    pw_act(v[2], a.act), pw_act(v[3], a.act));
+    } else {
+        if (a.res) {
+            const uint2 u = *(const uint2*)((const T*)a.res + off);
+            T rr[4];
+            __builtin_memcpy(rr, &u, 8);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] += (float)rr[r];
+        }
+        T e[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) e[r] = (T)pw_act(v[r], a.act);
+        uint2 u;
+        __builtin_memcpy(&u, e, 8);
+        *(uint2*)((T*)a.y + off) = u;
+    }
 }
 
 // Block: PW_WAVES waves on output channels [co0, co0 + 16 CF); blockIdx.y is
@@ -136,23 +192,90 @@ __global__ void __launch_bounds__(PW_WAVES * 64) pw_conv_kernel(ConvGemmArgs a)
                 const int c = 16 * f + cl, co = co0 + c;
                 if (co >= a.Co)
                     break;
-                const size_t off = (size_t)p * a.Co + co;
-                float v[4];
+                pw_store4<T>(a, p, co, c, acc[f], s_scale, s_bias);
+            }
+        }
+    }
+}
+
+// Stem: block of PW_WAVES waves on output channels [co0, co0 + 16 CF), KST
+// k-steps of four taps (taps past KH KW have zero weights and load nothing).
+template <typename T, int CF, int KST>
+__global__ void __launch_bounds__(PW_WAVES * 64) stem_conv_kernel(ConvGemmArgs a)
+{
+    constexpr int ESZ = (int)sizeof(T);
+    constexpr int EPV = 16 / ESZ;
+    constexpr int ROWS = CF * 16;
+    __shared__ float s_scale[ROWS], s_bias[ROWS];
+    // weights [ks][row][4 taps x 16 bytes]: a fragment read is 1 KB contiguous
+    __shared__ uint4 s_w[KST * ROWS * 4];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int co0 = blockIdx.y * ROWS;
+    for (int i = tid; i < ROWS; i += PW_WAVES * 64) {
+        const bool in = co0 + i < a.Co;
+        s_scale[i] = in ? a.scale[co0 + i] : 0.0f;
+        s_bias[i] = in ? a.bias[co0 + i] : 0.0f;
+    }
+    const auto wsrc = pw_rsrc(a.w, (uint32_t)a.Co * a.Kpad * ESZ);
+    for (int i = tid; i < KST * ROWS * 4; i += PW_WAVES * 64) {
+        const int q = i & 3, r = (i >> 2) % ROWS, ks = (i >> 2) / ROWS;
+        const int row = co0 + r, k = (4 * ks + q) * EPV;
+        s_w[i] = pw_load16(wsrc, row < a.Co && k < a.Kpad ? (uint32_t)((row * a.Kpad + k) * ESZ)
+                                                          : PW_OOB);
+    }
+    __syncthreads();
+
+    const auto xsrc = pw_rsrc(a.x, (uint32_t)a.N * a.H * a.W * a.C * ESZ);
+    const int taps = a.KH * a.KW, hw = a.Ho * a.Wo;
+    const int groups = (a.M + 15) / 16;
+    const int stride = gridDim.x * PW_WAVES;
+    const int q = lane >> 4, cl = 4 * q;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    for (int g = blockIdx.x * PW_WAVES + wave; g < groups; g += stride) {
+        const int p = g * 16 + (lane & 15);
+        const int n = p / hw, rem = p - n * hw;
+        const int ho = rem / a.Wo, wo = rem - (rem / a.Wo) * a.Wo;
+        const int h0 = ho * a.stride - a.pad, w0 = wo * a.stride - a.pad;
+        // gather: this lane group's tap of every k-step, C channels each
+        uint32_t e[KST][4];
 #pragma unroll
-                for (int r = 0; r < 4; ++r) v[r] = acc[f][r] * s_scale[c + r] + s_bias[c + r];
-                if (a.res) {
-                    const uint2 u = *(const uint2*)((const T*)a.res + off);
-                    T rr[4];
-                    __builtin_memcpy(rr, &u, 8);
+        for (int ks = 0; ks < KST; ++ks) {
+            const int t = 4 * ks + q;
+            const int kh = t / a.KW, kw = t - (t / a.KW) * a.KW;
+            const int hi = h0 + kh, wi = w0 + kw;
+            const bool ok = p < a.M && t < taps && hi >= 0 && hi < a.H && wi >= 0 && wi < a.W;
+            const uint32_t base = (uint32_t)((((n * a.H + hi) * a.W + wi) * a.C) * ESZ);
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) v[r] += (float)rr[r];
-                }
-                T e[4];
+            for (int ci = 0; ci < 4; ++ci) {
+                const uint32_t off = ok && ci < a.C ? base + ci * ESZ : PW_OOB;
+                if constexpr (ESZ == 4)
+                    e[ks][ci] = __builtin_amdgcn_raw_buffer_load_b32(xsrc, off, 0, 0);
+                else
+                    e[ks][ci] = __builtin_amdgcn_raw_buffer_load_b16(xsrc, off, 0, 0);
+            }
+        }
+        floatx4 acc[CF];
 #pragma unroll
-                for (int r = 0; r < 4; ++r) e[r] = (T)pw_act(v[r], a.act);
-                uint2 u;
-                __builtin_memcpy(&u, e, 8);
-                *(uint2*)((T*)a.y + off) = u;
+        for (int f = 0; f < CF; ++f) acc[f] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int ks = 0; ks < KST; ++ks) {
+            uint4 b;
+            if constexpr (ESZ == 4)
+                b = uint4{e[ks][0], e[ks][1], e[ks][2], e[ks][3]};
+            else
+                b = uint4{e[ks][0] | (e[ks][1] << 16), e[ks][2] | (e[ks][3] << 16), 0u, 0u};
+#pragma unroll
+            for (int f = 0; f < CF; ++f)
+                acc[f] = pw_mfma<T>(s_w[(ks * ROWS + 16 * f + (lane & 15)) * 4 + q], b, acc[f]);
+        }
+        if (p < a.M) {
+#pragma unroll
+            for (int f = 0; f < CF; ++f) {
+                const int c = 16 * f + cl, co = co0 + c;
+                if (co >= a.Co)
+                    break;
+                pw_store4<T>(a, p, co, c, acc[f], s_scale, s_bias);
             }
         }
     }
@@ -195,7 +318,71 @@ hipError_t launch_pw_dt(int cf, const ConvGemmArgs& a, int grid_blocks, hipStrea
     }
 }
 
+template <typename T, int CF, int KST>
+hipError_t launch_stem_t(const ConvGemmArgs& a, int grid_blocks, hipStream_t s)
+{
+    static int resident = 0;
+    if (!resident) {
+        int n = 0;
+        const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &n, stem_conv_kernel<T, CF, KST>, PW_WAVES * 64, 0);
+        if (e != hipSuccess)
+            return e;
+        resident = std::max(1, n);
+    }
+    const int groups = (a.M + 15) / 16;
+    const int slices = (a.Co + CF * 16 - 1) / (CF * 16);
+    const int cap = grid_blocks > 0 ? grid_blocks
+                                    : std::max(NUM_CUS_PW * resident / slices, NUM_CUS_PW);
+    const int gx = std::min((groups + PW_WAVES - 1) / PW_WAVES, cap);
+    const dim3 grid((unsigned)gx, (unsigned)slices), block(PW_WAVES * 64);
+    PPIPE_LAUNCH((stem_conv_kernel<T, CF, KST>), grid, block, 0, s, a);
+    return hipGetLastError();
+}
+
+template <typename T, int CF>
+hipError_t launch_stem_cf(const ConvGemmArgs& a, int grid_blocks, hipStream_t s)
+{
+    const int kst = (a.KH * a.KW + 3) / 4;
+    if (kst <= 3) return launch_stem_t<T, CF, 3>(a, grid_blocks, s);
+    if (kst <= 7) return launch_stem_t<T, CF, 7>(a, grid_blocks, s);
+    if (kst <= 13) return launch_stem_t<T, CF, 13>(a, grid_blocks, s);
+    return hipErrorInvalidValue;
+}
+
+template <typename T>
+hipError_t launch_stem_dt(int cf, const ConvGemmArgs& a, int grid_blocks, hipStream_t s)
+{
+    switch (cf) {
+    case 1:  return launch_stem_cf<T, 1>(a, grid_blocks, s);
+    case 2:  return launch_stem_cf<T, 2>(a, grid_blocks, s);
+    case 4:  return launch_stem_cf<T, 4>(a, grid_blocks, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
 }  // namespace
+
+int stem_channel_frags(int Co)
+{
+    // slices of at most 64 output channels, split evenly
+    const int slices = (Co + 63) / 64;
+    const int need = (Co + 16 * slices - 1) / (16 * slices);
+    return need <= 1 ? 1 : need <= 2 ? 2 : 4;
+}
+
+hipError_t launch_stem(int dt, int cf, const ConvGemmArgs& a, int grid_blocks, hipStream_t s)
+{
+    if (a.C > 4 || a.C >= 16 / dtype_size(dt) || a.Co % 4 != 0 || a.KH * a.KW > 52 ||
+        a.softmax || a.splits != 1)
+        return hipErrorInvalidValue;
+    switch (dt) {
+    case DT_F32:  return launch_stem_dt<float>(cf, a, grid_blocks, s);
+    case DT_F16:  return launch_stem_dt<_Float16>(cf, a, grid_blocks, s);
+    case DT_BF16: return launch_stem_dt<__bf16>(cf, a, grid_blocks, s);
+    default:      return hipErrorInvalidValue;
+    }
+}
 
 int pointwise_channel_frags(int Co)
 {

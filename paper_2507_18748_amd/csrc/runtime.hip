@@ -111,6 +111,7 @@ struct LayerRT {
     int kind;
     bool tapv = false, softmax = false, skinny_ok = false, pad_in = false;
     bool pw_ok = false;         // the streaming 1x1 kernel applies (GEMM_PW)
+    bool stem_ok = false;       // the stem kernel applies (GEMM_STEM)
     int KH = 1, KW = 1, gstride = 1, gpad = 0, K = 0, Kpad = 0;
     int cpad = 0;               // channels as the GEMM reads them (C rounded up to a vector)
     size_t w_off = 0, scale_off = 0, bias_off = 0;
@@ -169,7 +170,7 @@ namespace {
 // shape, waves per tile (skinny) and tile order.  Deterministic in (M, Co, K,
 // dtype, eligibility) so that the latency table, the benchmark and the
 // parity tests exercise the same launches.
-Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok)
+Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool stem_ok)
 {
     auto tiles = [&](int cfg) {
         GemmCfgInfo c = gemm_cfg_info(cfg);
@@ -230,6 +231,17 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok)
         wk = pointwise_channel_frags(Co);
         splits = 1;
     }
+    //  * stems of 3-channel images take the stem kernel (no channel-padding
+    //    pass): filters of up to 28 taps always (3x3 stems 1.7-2.4x faster),
+    //    7x7 stems only on small grids (its 13 k-steps of gathered taps
+    //    leave one wave per SIMD; the padded GEMM is ahead from about
+    //    200k output pixels).  PPIPE_GEMM_NO_STEM turns it off for A/B timing.
+    const int taps = K / (16 / dtype_size(dt));
+    if (stem_ok && (taps <= 28 || M <= 65536) && !std::getenv("PPIPE_GEMM_NO_STEM")) {
+        cfg = GEMM_STEM;
+        wk = stem_channel_frags(Co);
+        splits = 1;
+    }
     // PPIPE_GEMM_PLAN="cfg,waves,splits" forces one configuration on every
     // eligible GEMM layer (tuning sweeps and kernel tests).
     if (const char* env = std::getenv("PPIPE_GEMM_PLAN")) {
@@ -241,6 +253,12 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok)
                 if (pw_ok) {
                     cfg = fc;
                     wk = pointwise_channel_frags(Co);
+                    splits = 1;
+                }
+            } else if (fc == GEMM_STEM) {
+                if (stem_ok) {
+                    cfg = fc;
+                    wk = stem_channel_frags(Co);
                     splits = 1;
                 }
             } else if (!sk) {
@@ -263,7 +281,7 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok)
     p.splits = (p.total_chunks + p.chunks_per_split - 1) / p.chunks_per_split;
     p.tiles_m = (M + c.bn - 1) / c.bn;
     p.tiles_co = (Co + c.bm - 1) / c.bm;
-    if (cfg == GEMM_PW) {   // 16-pixel groups x output-channel slices of wk fragments
+    if (cfg == GEMM_PW || cfg == GEMM_STEM) {   // 16-pixel groups x channel slices of wk fragments
         p.tiles_co = (Co + 16 * wk - 1) / (16 * wk);
         if (const char* env = std::getenv("PPIPE_PW_GRID"))   // tuning sweeps
             p.grid = std::max(0, std::atoi(env));
@@ -276,7 +294,13 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok)
 // planned on the skinny kernel has whole K steps per tap (skinny_ok).
 bool tapv_of(const LayerRT& l, const Plan& p)
 {
-    return l.tapv && !gemm_cfg_info(p.cfg).skinny;
+    return l.tapv && !gemm_cfg_info(p.cfg).skinny && p.cfg != GEMM_PW && p.cfg != GEMM_STEM;
+}
+
+// The stem kernel reads the image itself; other kernels read it channel-padded.
+bool pads_input(const LayerRT& l, const Plan& p)
+{
+    return l.pad_in && p.cfg != GEMM_STEM;
 }
 
 const void* buf_ptr(const ppipe_partition* P, int id, const void* in, void* out)
@@ -319,7 +343,7 @@ std::vector<int> launch_roles(const LayerRT& l, int batch)
 {
     if (l.kind != K_GEMM) return {L_OTHER};
     std::vector<int> r;
-    if (l.pad_in) r.push_back(L_PAD);
+    if (pads_input(l, l.plans[batch - 1])) r.push_back(L_PAD);
     r.push_back(L_GEMM);
     // the softmax launch of an FC + softmax layer also reduces its K splits
     if (l.plans[batch - 1].splits > 1 && !l.softmax) r.push_back(L_REDUCE);
@@ -382,7 +406,8 @@ hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, 
         const std::vector<int> roles = launch_roles(l, batch);
         auto want = [&](int i) { return only < 0 || only == i; };
         int li = 0;
-        if (l.pad_in) {
+        const bool pad = pads_input(l, p);
+        if (pad) {
             if (want(li)) {
                 if (hook) hook->before(l, li, s);
                 e = launch_pad_channels(P->dtype, x, P->pad_buf, (size_t)batch * l.H * l.W, l.C,
@@ -393,7 +418,7 @@ hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, 
             ++li;
         }
         ConvGemmArgs a;
-        a.x = l.pad_in ? (const void*)P->pad_buf : x;
+        a.x = pad ? (const void*)P->pad_buf : x;
         a.w = l.w;
         a.scale = l.scale;
         a.bias = l.bias;
@@ -403,7 +428,7 @@ hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, 
         a.partial = P->ws;
         a.logits = P->ws + (p.splits > 1 ? (size_t)p.splits * a.M * l.Co : 0);
         a.N = batch;
-        a.H = l.H; a.W = l.W; a.C = l.cpad;
+        a.H = l.H; a.W = l.W; a.C = pad ? l.cpad : l.C;
         a.Ho = l.Ho; a.Wo = l.Wo; a.Co = l.Co;
         a.KH = l.KH; a.KW = l.KW; a.stride = l.gstride; a.pad = l.gpad;
         a.K = l.K; a.Kpad = l.Kpad;
@@ -673,6 +698,8 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
             // streaming 1x1 kernel: 16-bit, stride 1, unpadded, one MFMA k-step
             l.pw_ok = dt != DT_F32 && ld.op == PPIPE_OP_CONV && l.KH * l.KW == 1 &&
                       l.gstride == 1 && l.gpad == 0 && !l.pad_in && x.c <= 32;
+            // stem kernel: an image of at most 4 channels (below one vector), <= 52 taps
+            l.stem_ok = ld.op == PPIPE_OP_CONV && l.pad_in && x.c <= 4 && l.KH * l.KW <= 52;
             if (l.tapv && l.Kpad / epv > GEMM_VTAB_MAX)
                 return fail(PPIPE_E_UNSUPPORTED, who + ": reduction length " +
                                                      std::to_string(l.K) + " with C = " +
@@ -815,7 +842,7 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
         l.plans.resize(P->max_batch);
         for (int b = 1; b <= P->max_batch; ++b) {
             const int M = b * l.Ho * l.Wo;
-            const Plan p = choose_plan(M, l.Co, l.K, dt, l.skinny_ok, l.pw_ok);
+            const Plan p = choose_plan(M, l.Co, l.K, dt, l.skinny_ok, l.pw_ok, l.stem_ok);
             l.plans[b - 1] = p;
             size_t need = 0;
             if (p.splits > 1) need += (size_t)p.splits * M * l.Co;
@@ -825,8 +852,10 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
     }
     P->ws_bytes = ws;
     for (const LayerRT& l : P->L)
-        if (l.kind == K_GEMM && l.pad_in)
-            P->pad_bytes = std::max(P->pad_bytes, (size_t)P->max_batch * l.H * l.W * l.cpad * esz);
+        if (l.kind == K_GEMM)
+            for (int b = 1; b <= P->max_batch; ++b)
+                if (pads_input(l, l.plans[b - 1]))
+                    P->pad_bytes = std::max(P->pad_bytes, (size_t)b * l.H * l.W * l.cpad * esz);
     const LayerRT& last = P->L.back();
     P->in = shape_of(d->layers[begin].src);
     P->out = {last.Co, last.Ho, last.Wo};

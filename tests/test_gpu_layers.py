@@ -83,6 +83,35 @@ def test_pointwise_kernel(monkeypatch, dtype, ci, co, h, w, batch, res, act):
     check(m, dtype, batch)
 
 
+# Stems: (C, Co, k, stride, pad, H, W, batch) of images with C <= 4 channels.
+STEM_CASES = [
+    (3, 64, 3, 1, 1, 19, 17, 2),    # VGG conv1_1
+    (3, 32, 3, 2, 1, 23, 21, 3),    # MobileNetV2 stem
+    (3, 64, 7, 2, 3, 29, 27, 2),    # ResNet stem
+    (3, 36, 5, 1, 2, 11, 13, 2),    # ragged channel slice, 25 taps
+    (1, 16, 3, 1, 0, 9, 8, 3),      # one channel, no padding
+    (3, 100, 7, 2, 3, 15, 15, 1),   # two channel slices
+]
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("ci,co,k,st,pd,h,w,batch", STEM_CASES)
+def test_stem_kernel(dtype, ci, co, k, st, pd, h, w, batch):
+    from paper_2507_18748_amd import Partition
+    m = make((ci, h, w), [conv("s", -1, ci, co, k, st, pd)])
+    with Partition(m.layers, W.model_params(m, 0, dtype), (ci, h, w), 0, 1, dtype,
+                   max_batch=batch) as part:
+        assert part.layer_info(0, batch)["kernel"].startswith("stem_conv<")
+    check(m, dtype, batch, kind="image" if ci == 3 else "normal")
+
+
+def test_stem_kernel_four_channels():
+    """A 4-channel 16-bit image (below one 8-element vector) takes the stem
+    kernel too."""
+    m = make((4, 12, 10), [conv("s", -1, 4, 32, 3, 1, 1)])
+    check(m, "bf16", 2)
+
+
 @pytest.mark.parametrize("grid", ["1", "8"])
 def test_pointwise_grid_stride_matches_default(monkeypatch, grid):
     """A pointwise launch capped at 1 or 8 blocks (every wave walks many
