@@ -787,22 +787,32 @@ conv_gemm_dma(ConvGemmArgs a)
 
 // Split-K reduction: one thread per 4 output channels of one pixel, partials
 // summed in split order (bitwise deterministic), then the layer epilogue.
+// The loads of four splits are issued before the first add (a load past the
+// last split reads zeros through the range check and is not added), so the
+// split latencies overlap instead of adding up.
 template <typename T>
 __global__ void __launch_bounds__(256) splitk_reduce_kernel(ConvGemmArgs a)
 {
-    const size_t nvec = (size_t)a.M * a.Co / 4;
-    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const uint32_t nvec = (uint32_t)a.M * a.Co / 4;
+    const uint32_t i = blockIdx.x * 256u + threadIdx.x;
     if (i >= nvec)
         return;
-    const float4* p = (const float4*)a.partial;
-    float4 t = p[i];
-    for (int sp = 1; sp < a.splits; ++sp) {
-        const float4 v = p[(size_t)sp * nvec + i];
-        t.x += v.x; t.y += v.y; t.z += v.z; t.w += v.w;
+    const auto src = make_rsrc(a.partial, (uint32_t)a.splits * nvec * 16u);
+    const uint32_t plane = nvec * 16u;
+    floatx4 t = __builtin_bit_cast(floatx4, buf_load16(src, i * 16u));
+    for (int sp0 = 1; sp0 < a.splits; sp0 += 4) {
+        uint4 u[4];
+#pragma unroll
+        for (int d = 0; d < 4; ++d)
+            u[d] = buf_load16(src, sp0 + d < a.splits ? (uint32_t)(sp0 + d) * plane + i * 16u : OOB);
+#pragma unroll
+        for (int d = 0; d < 4; ++d)
+            if (sp0 + d < a.splits)
+                t += __builtin_bit_cast(floatx4, u[d]);
     }
-    const int co = (int)((i * 4) % (size_t)a.Co);
-    const int m = (int)((i * 4) / (size_t)a.Co);
-    store_out4<T>(a, co, m, floatx4{t.x, t.y, t.z, t.w});
+    const int co = (int)((i * 4u) % (uint32_t)a.Co);
+    const int m = (int)((i * 4u) / (uint32_t)a.Co);
+    store_out4<T>(a, co, m, t);
 }
 
 // Skinny implicit GEMM for layers with few output pixels.
@@ -1144,6 +1154,8 @@ const char* softmax_rows_name() { return "softmax_rows<f32>"; }
 hipError_t launch_splitk_reduce(int dt, const ConvGemmArgs& a, hipStream_t s)
 {
     const size_t nvec = (size_t)a.M * a.Co / 4;
+    if ((double)a.splits * nvec * 16.0 >= 2147483648.0)   // 32-bit buffer offsets
+        return hipErrorInvalidValue;
     const dim3 grid((unsigned)((nvec + 255) / 256)), block(256);
     switch (dt) {
     case DT_F32:
