@@ -185,7 +185,8 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
     //    hundred of them split over K;
     //  * everything else takes 64x64 tiles; K is split only when each half
     //    keeps >= 12 steps, then while the grid is short of about 1.5 blocks
-    //    per CU and each split keeps >= 4 steps;
+    //    per CU and each split keeps >= 4 steps, or up to 2 blocks per CU
+    //    with >= 12 steps per split;
     //  * sparse grids (under two 64x64 blocks, or one 8-wave 128x128 block,
     //    per CU) take software-pipelined loops; sparse 64x64 grids use 8
     //    waves and four stages (two in flight), because a lone block streams
@@ -215,7 +216,7 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
             const int cps = k / (splits * 2);
             const bool ok = splits == 1 ? (cps >= 12 && nb <= 384)
                                         : ((nb <= 128 && cps >= 2) || (nb <= 384 && cps >= 4) ||
-                                           (nb <= 512 && cps >= 8));
+                                           (nb <= 512 && cps >= 12));
             if (!ok) break;
             splits *= 2;
         }
