@@ -98,13 +98,14 @@ def cold_summary(records, dtype):
 
 
 def source_digest():
-    """sha256 over the kernel and runtime sources, the HIP files and their
-    shared header (any change invalidates HBM counters taken before it; the
-    host-only request scheduler is not part of it)."""
+    """sha256 over the sources that define the GEMM kernel whose HBM counters
+    are recorded and the planner that configures it (conv_gemm.hip,
+    kernels.h, runtime.hip): a change to any of them invalidates counters
+    taken before it."""
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2507_18748_amd", "csrc")
-    for f in sorted(x for x in os.listdir(csrc) if x.endswith((".hip", ".h"))):
+    for f in ("conv_gemm.hip", "kernels.h", "runtime.hip"):
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + b"\0" + fh.read())
     return h.hexdigest()

@@ -367,12 +367,18 @@ hipError_t launch_dwconv(int dt, const void* x, const void* w, const float* scal
     if (k != 3 || (stride != 1 && stride != 2))
         return hipErrorInvalidValue;
     const int cv = C / (16 / dtype_size(dt));
-    const int pw = stride == 1 ? 4 : 2;
+    // outputs per thread along a row: 4 on wide stride-1 maps, else 2 (more
+    // threads on small maps, fewer registers: 166 against 194 VGPRs)
+    const int pw = stride == 1 && Wo >= 96 ? 4 : 2;
     const size_t total = (size_t)N * Ho * ((Wo + pw - 1) / pw) * cv;
     if (total >= (1u << 31) || (double)N * H * W * C * dtype_size(dt) >= 2147483648.0)
         return hipErrorInvalidValue;
-    if (stride == 1) {
+    if (stride == 1 && pw == 4) {
         PPIPE_DISPATCH(dt, PPIPE_LAUNCH((dwconv3_kernel<T, 1, 4>), dim3(blocks_for(total)),
+                                        dim3(256), 0, s, (const T*)x, (const T*)w, scale,
+                                        bias, (T*)y, N, H, W, C, Ho, Wo, pad, act));
+    } else if (stride == 1) {
+        PPIPE_DISPATCH(dt, PPIPE_LAUNCH((dwconv3_kernel<T, 1, 2>), dim3(blocks_for(total)),
                                         dim3(256), 0, s, (const T*)x, (const T*)w, scale,
                                         bias, (T*)y, N, H, W, C, Ho, Wo, pad, act));
     } else {

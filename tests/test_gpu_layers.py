@@ -174,7 +174,7 @@ def test_stem3x3_relu6_gather(dtype):
 
 @pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("stride", [1, 2])
-@pytest.mark.parametrize("chw", [(96, 13, 13), (24, 9, 11), (8, 5, 6), (40, 2, 3)])
+@pytest.mark.parametrize("chw", [(96, 13, 13), (24, 9, 11), (8, 5, 6), (40, 2, 3), (16, 3, 101)])
 def test_depthwise3x3(dtype, stride, chw):
     """Ragged output rows (the last pixel group of a row is partial), one and
     several channel vectors, maps narrower than a pixel group."""
