@@ -947,29 +947,34 @@ softmax_rows_kernel(const float* __restrict__ z, int splits, const float* __rest
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     const int m = blockIdx.x;
     const size_t plane = (size_t)M * O;
-    const float* zr = z + (size_t)m * O;
-    // Split sums in split order; the loads of up to four splits are issued
-    // before their additions so that the row's memory latency overlaps.
+    // Split sums in split order; the loads of up to eight splits (the first
+    // included) are issued before their additions, through the buffer range
+    // check (past the row or the last split: zeros, not added), so that the
+    // row's memory latency is paid once per eight splits.
+    constexpr int G = VPT <= 8 ? 8 : 2;
+    const auto zs = make_rsrc(z, (uint32_t)((size_t)splits * plane * 4));
     float v[VPT];
+    for (int sp0 = 0; sp0 < splits; sp0 += G) {
+        float u[G][VPT];
 #pragma unroll
-    for (int q = 0; q < VPT; ++q) {
-        const int o = t + q * 256;
-        v[q] = o < O ? zr[o] : 0.0f;
-    }
-    for (int sp0 = 1; sp0 < splits; sp0 += 4) {
-        float u[4][VPT];
-#pragma unroll
-        for (int d = 0; d < 4; ++d)
+        for (int d = 0; d < G; ++d)
 #pragma unroll
             for (int q = 0; q < VPT; ++q) {
                 const int o = t + q * 256;
-                u[d][q] = (sp0 + d < splits && o < O) ? zr[(sp0 + d) * plane + o] : 0.0f;
+                const uint32_t off = sp0 + d < splits && o < O
+                                         ? (uint32_t)(((sp0 + d) * plane + (size_t)m * O + o) * 4)
+                                         : OOB;
+                u[d][q] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(zs, off, 0, 0));
             }
 #pragma unroll
-        for (int d = 0; d < 4; ++d)
+        for (int d = 0; d < G; ++d)
 #pragma unroll
-            for (int q = 0; q < VPT; ++q)
-                if (sp0 + d < splits) v[q] += u[d][q];
+            for (int q = 0; q < VPT; ++q) {
+                if (sp0 + d == 0)
+                    v[q] = u[0][q];
+                else if (sp0 + d < splits)
+                    v[q] += u[d][q];
+            }
     }
     float mx = -INFINITY;
 #pragma unroll

@@ -200,34 +200,50 @@ maxpool_kernel(const T* __restrict__ x, T* __restrict__ y, int N, int H, int W, 
     Vec16<T>::store(y + (((size_t)n * Ho + ho) * Wo + wo) * C + c, m);
 }
 
-// Global average pool: a block owns 32 channel vectors (256 or 128 channels)
-// of one image; its 8 thread rows split the H*W pixels, so every pixel row of
-// the block is one contiguous 512-byte read, and the 8 partial sums are added
-// through LDS in a fixed order.
+// Global average pool: a block owns 16 channel vectors (128 or 64 channels)
+// of one image; its 16 thread rows split the H*W pixels (every 16th pixel per
+// thread, loads issued four at a time), so every pixel row of the block is
+// one contiguous 256-byte read, and the 16 partial sums are added through LDS
+// in a fixed order.
 template <typename T>
 __global__ void __launch_bounds__(256)
 gap_kernel(const T* __restrict__ x, T* __restrict__ y, int N, int HW, int C)
 {
     constexpr int V = Vec16<T>::N;
-    __shared__ float part[8][32][V + 1];
+    constexpr int ESZ = (int)sizeof(T);
+    constexpr uint32_t OOB = 0x80000000u;
+    __shared__ float part[16][16][V + 1];
     const int CV = C / V;
-    const int cv = blockIdx.x % ((CV + 31) / 32) * 32 + (threadIdx.x & 31);
-    const int n = blockIdx.x / ((CV + 31) / 32);
-    const int pr = threadIdx.x >> 5;    // pixel row 0..7
+    const int cg = (CV + 15) / 16;
+    const int cv = blockIdx.x % cg * 16 + (threadIdx.x & 15);
+    const int n = blockIdx.x / cg;
+    const int pr = threadIdx.x >> 4;    // pixel row 0..15
+    const auto xr = dw_rsrc(x, (uint32_t)N * HW * C * ESZ);
     float s[V];
 #pragma unroll
     for (int i = 0; i < V; ++i) s[i] = 0.0f;
     if (cv < CV) {
-        const T* p = x + (size_t)n * HW * C + cv * V;
-        for (int t = pr; t < HW; t += 8) {
-            float v[V];
-            Vec16<T>::load(p + (size_t)t * C, v);
+        const uint32_t base = (uint32_t)(((size_t)n * HW * C + (size_t)cv * V) * ESZ);
+        for (int t0 = pr; t0 < HW; t0 += 64) {
+            uint4 u[4];
 #pragma unroll
-            for (int i = 0; i < V; ++i) s[i] += v[i];
+            for (int d = 0; d < 4; ++d) {
+                const int t = t0 + 16 * d;
+                u[d] = dw_load(xr, t < HW ? base + (uint32_t)(t * C * ESZ) : OOB);
+            }
+#pragma unroll
+            for (int d = 0; d < 4; ++d) {
+                if (t0 + 16 * d >= HW)
+                    break;
+                float v[V];
+                unpack16<T>(u[d], v);
+#pragma unroll
+                for (int i = 0; i < V; ++i) s[i] += v[i];
+            }
         }
     }
 #pragma unroll
-    for (int i = 0; i < V; ++i) part[pr][threadIdx.x & 31][i] = s[i];
+    for (int i = 0; i < V; ++i) part[pr][threadIdx.x & 15][i] = s[i];
     __syncthreads();
     if (pr == 0 && cv < CV) {
         const float inv = 1.0f / (float)HW;
@@ -235,7 +251,7 @@ gap_kernel(const T* __restrict__ x, T* __restrict__ y, int N, int HW, int C)
 #pragma unroll
         for (int i = 0; i < V; ++i) {
             float t = 0.0f;
-            for (int r = 0; r < 8; ++r) t += part[r][threadIdx.x][i];
+            for (int r = 0; r < 16; ++r) t += part[r][threadIdx.x][i];
             o[i] = t * inv;
         }
         Vec16<T>::store(y + (size_t)n * C + cv * V, o);
@@ -402,7 +418,9 @@ hipError_t launch_maxpool(int dt, const void* x, void* y, int N, int H, int W, i
 hipError_t launch_gap(int dt, const void* x, void* y, int N, int HW, int C, hipStream_t s)
 {
     const int CV = C / (16 / dtype_size(dt));
-    const unsigned blocks = (unsigned)N * ((CV + 31) / 32);
+    const unsigned blocks = (unsigned)N * ((CV + 15) / 16);
+    if ((double)N * HW * C * dtype_size(dt) >= 2147483648.0)   // 32-bit buffer offsets
+        return hipErrorInvalidValue;
     PPIPE_DISPATCH(dt, PPIPE_LAUNCH(gap_kernel<T>, dim3(blocks), dim3(256), 0, s,
                                           (const T*)x, (T*)y, N, HW, C));
     return hipGetLastError();
