@@ -68,6 +68,18 @@ __device__ __forceinline__ uint4 dw_load(__amdgpu_buffer_rsrc_t r, uint32_t off)
 {
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
+// Block index with the grid spread over the 8 XCDs in contiguous ranges (the
+// hardware deals block b to XCD b % 8): neighbouring output rows, whose input
+// windows overlap, run on one XCD and share its L2 instead of each XCD
+// fetching the overlapping rows again.
+__device__ __forceinline__ uint32_t xcd_block()
+{
+    constexpr uint32_t XCDS = 8;
+    const uint32_t G = gridDim.x, b = blockIdx.x;
+    const uint32_t xcd = b % XCDS, slot = b / XCDS, per = G / XCDS, rem = G % XCDS;
+    return xcd * per + (xcd < rem ? xcd : rem) + slot;
+}
+
 template <typename T>
 __device__ __forceinline__ void unpack16(const uint4& u, float* f)
 {
@@ -95,7 +107,7 @@ dwconv3_kernel(const T* __restrict__ x, const T* __restrict__ w, const float* __
     const int CV = C / V;
     const int WQ = (Wo + PW - 1) / PW;
     const uint32_t total = (uint32_t)N * Ho * WQ * CV;
-    const uint32_t idx = blockIdx.x * 256u + threadIdx.x;
+    const uint32_t idx = xcd_block() * 256u + threadIdx.x;
     if (idx >= total)
         return;
     const int cv = (int)(idx % CV);
@@ -170,7 +182,7 @@ maxpool_kernel(const T* __restrict__ x, T* __restrict__ y, int N, int H, int W, 
     constexpr int V = Vec16<T>::N;
     const int CV = C / V;
     const size_t total = (size_t)N * Ho * Wo * CV;
-    const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const size_t idx = (size_t)xcd_block() * blockDim.x + threadIdx.x;
     if (idx >= total)
         return;
     const int cv = (int)(idx % CV);
