@@ -90,7 +90,8 @@ enum GemmCfg : int {
     GEMM_DMA_64x64_8W_S3 = 14,    // 8 waves, 3 stages, software-pipelined
     GEMM_DMA_64x64_8W_S4 = 15,    // 8 waves, 4 stages (two in flight)
     GEMM_DMA_64x64_8W_S6 = 16,    // 8 waves, 6 stages (four in flight; few blocks per CU)
-    // Streaming 1x1 convolution (stride 1, C <= 32): weights in registers,
+    // Streaming 1x1 convolution (stride 1, C <= 32, or <= 160 into <= 32
+    // channels): weights in registers,
     // 16-pixel groups loaded straight into MFMA fragments.  wk = 16-channel
     // fragments per block (pointwise_channel_frags).
     GEMM_PW = 17,
@@ -126,8 +127,9 @@ hipError_t launch_conv_gemm(int dt, int cfg, int wk, bool tapv, const ConvGemmAr
                             hipStream_t s);
 const char* conv_gemm_name(int dt, int cfg, int wk, bool tapv);
 
-// Streaming 1x1 convolution (GEMM_PW) of a 16-bit layer with C <= 32 (a
-// multiple of 8), Co % 4 == 0, stride 1, no padding, no K split, no softmax;
+// Streaming 1x1 convolution (GEMM_PW) of a 16-bit layer with C <= 32, or
+// C <= 160 with cf <= 2 (C a multiple of 8), Co % 4 == 0, stride 1, no
+// padding, no K split, no softmax;
 // cf 16-channel fragments per block, at most grid_blocks blocks along the
 // pixels (0: one resident set), each wave walking 16-pixel groups grid-stride.
 hipError_t launch_pointwise(int dt, int cf, const ConvGemmArgs& a, int grid_blocks, hipStream_t s);

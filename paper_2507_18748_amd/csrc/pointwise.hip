@@ -3,10 +3,11 @@
 //
 // Pointwise (GEMM_PW).
 // A 1x1, stride-1 convolution with C <= 32 input channels reduces over one
-// 32-element MFMA k-step per output, so the GEMM's machinery (K loop, LDS
-// stage ring, staged epilogue) is overhead: these layers (the expansion and
-// projection convolutions of MobileNetV2's early blocks) are bound by
-// streaming their input and output through HBM.  Here each wave keeps the
+// 32-element MFMA k-step per output (up to five with at most 32 output
+// channels), so the GEMM's machinery (K loop, LDS stage ring, staged
+// epilogue) is overhead: these layers (the expansion and projection
+// convolutions of MobileNetV2's early blocks) are bound by streaming their
+// input and output through HBM.  Here each wave keeps the
 // weights of its block's output-channel slice (at most 96 channels, to keep
 // registers, and so resident waves, in check) in registers as MFMA A
 // fragments and walks 16-pixel groups of the NHWC input grid-stride, in a
@@ -43,7 +44,6 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 constexpr int NUM_CUS_PW = 256;            // MI355X compute units
 constexpr uint32_t PW_OOB = 0x80000000u;   // beyond any buffer: the load returns zeros
 constexpr int PW_WAVES = 4;
-constexpr int PW_PF = 3;                   // groups in flight ahead of the one computed
 
 template <typename T> __device__ __forceinline__ floatx4 pw_mfma(uint4 a, uint4 b, floatx4 c);
 template <> __device__ __forceinline__ floatx4 pw_mfma<_Float16>(uint4 a, uint4 b, floatx4 c)
@@ -121,10 +121,12 @@ __device__ __forceinline__ void pw_store4(const ConvGemmArgs& a, int p, int co, 
 
 // Block: PW_WAVES waves on output channels [co0, co0 + 16 CF); blockIdx.y is
 // the channel slice, waves of all blocks along x share the pixel groups.
-// KS: 32-element k-steps (C <= 32 KS).
+// KS: 32-element k-steps (C <= 32 KS); groups in flight ahead of the one
+// computed: 3 with one k-step, 1 with more (registers).
 template <typename T, int CF, int KS>
 __global__ void __launch_bounds__(PW_WAVES * 64) pw_conv_kernel(ConvGemmArgs a)
 {
+    constexpr int PW_PF = KS == 1 ? 3 : 1;
     constexpr int ESZ = (int)sizeof(T);
     __shared__ float s_scale[CF * 16], s_bias[CF * 16];
 
@@ -281,7 +283,7 @@ __global__ void __launch_bounds__(PW_WAVES * 64) stem_conv_kernel(ConvGemmArgs a
     }
 }
 
-template <typename T, int CF>
+template <typename T, int CF, int KS>
 hipError_t launch_pw_t(const ConvGemmArgs& a, int grid_blocks, hipStream_t s)
 {
     // one resident set of blocks (the kernel's occupancy on every CU, split
@@ -291,7 +293,7 @@ hipError_t launch_pw_t(const ConvGemmArgs& a, int grid_blocks, hipStream_t s)
     if (!resident) {
         int n = 0;
         const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-            &n, pw_conv_kernel<T, CF, 1>, PW_WAVES * 64, 0);
+            &n, pw_conv_kernel<T, CF, KS>, PW_WAVES * 64, 0);
         if (e != hipSuccess)
             return e;
         resident = std::max(1, n);
@@ -302,20 +304,36 @@ hipError_t launch_pw_t(const ConvGemmArgs& a, int grid_blocks, hipStream_t s)
                                     : std::max(NUM_CUS_PW * resident / slices, NUM_CUS_PW);
     const int gx = std::min((groups + PW_WAVES - 1) / PW_WAVES, cap);
     const dim3 grid((unsigned)gx, (unsigned)slices), block(PW_WAVES * 64);
-    PPIPE_LAUNCH((pw_conv_kernel<T, CF, 1>), grid, block, 0, s, a);
+    PPIPE_LAUNCH((pw_conv_kernel<T, CF, KS>), grid, block, 0, s, a);
     return hipGetLastError();
 }
 
 template <typename T>
 hipError_t launch_pw_dt(int cf, const ConvGemmArgs& a, int grid_blocks, hipStream_t s)
 {
-    switch (cf) {
-    case 1:  return launch_pw_t<T, 1>(a, grid_blocks, s);
-    case 2:  return launch_pw_t<T, 2>(a, grid_blocks, s);
-    case 4:  return launch_pw_t<T, 4>(a, grid_blocks, s);
-    case 6:  return launch_pw_t<T, 6>(a, grid_blocks, s);
-    default: return hipErrorInvalidValue;
+    const int ks = (a.C + 31) / 32;
+    if (ks == 1) {
+        switch (cf) {
+        case 1:  return launch_pw_t<T, 1, 1>(a, grid_blocks, s);
+        case 2:  return launch_pw_t<T, 2, 1>(a, grid_blocks, s);
+        case 4:  return launch_pw_t<T, 4, 1>(a, grid_blocks, s);
+        case 6:  return launch_pw_t<T, 6, 1>(a, grid_blocks, s);
+        default: return hipErrorInvalidValue;
+        }
     }
+    // more k-steps: at most 32 output channels per block
+#define PPIPE_PW_KS(CF_)                                                                         \
+    switch (ks) {                                                                                \
+    case 2:  return launch_pw_t<T, CF_, 2>(a, grid_blocks, s);                                   \
+    case 3:  return launch_pw_t<T, CF_, 3>(a, grid_blocks, s);                                   \
+    case 4:  return launch_pw_t<T, CF_, 4>(a, grid_blocks, s);                                   \
+    case 5:  return launch_pw_t<T, CF_, 5>(a, grid_blocks, s);                                   \
+    default: return hipErrorInvalidValue;                                                        \
+    }
+    if (cf == 1) { PPIPE_PW_KS(1) }
+    if (cf == 2) { PPIPE_PW_KS(2) }
+#undef PPIPE_PW_KS
+    return hipErrorInvalidValue;
 }
 
 template <typename T, int CF, int KST>
@@ -397,7 +415,7 @@ int pointwise_channel_frags(int Co)
 
 hipError_t launch_pointwise(int dt, int cf, const ConvGemmArgs& a, int grid_blocks, hipStream_t s)
 {
-    if (a.C > 32 || a.C % 8 != 0 || a.Co % 4 != 0 || a.KH != 1 || a.KW != 1 || a.stride != 1 ||
+    if (a.C > (cf <= 2 ? 160 : 32) || a.C % 8 != 0 || a.Co % 4 != 0 || a.KH != 1 || a.KW != 1 || a.stride != 1 ||
         a.pad != 0 || a.softmax || a.splits != 1)
         return hipErrorInvalidValue;
     switch (dt) {

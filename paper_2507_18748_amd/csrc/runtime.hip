@@ -223,10 +223,11 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
         if (t * splits < 512)
             cfg = GEMM_DMA_64x64_8W_S4;
     }
-    //  * 16-bit 1x1 stride-1 layers with at most 32 input channels and at
-    //    least 16384 output pixels stream through the pointwise kernel (2-3x
-    //    faster on MobileNetV2's large expansion layers; the GEMM stays ahead
-    //    on small grids).  PPIPE_GEMM_NO_PW turns it off for A/B timing.
+    //  * 16-bit 1x1 stride-1 layers with at most 32 input channels (or 160
+    //    with at most 32 output channels) and at least 16384 output pixels
+    //    stream through the pointwise kernel (2-3x faster on MobileNetV2's
+    //    large expansion layers; the GEMM stays ahead on small grids).
+    //    PPIPE_GEMM_NO_PW turns it off for A/B timing.
     if (pw_ok && M >= 16384 && !std::getenv("PPIPE_GEMM_NO_PW")) {
         cfg = GEMM_PW;
         wk = pointwise_channel_frags(Co);
@@ -697,8 +698,10 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
             // skinny kernel: each 64-byte K step lies in one (kh, kw) tap
             l.skinny_ok = l.KH * l.KW == 1 || l.cpad % (4 * epv) == 0;
             // streaming 1x1 kernel: 16-bit, stride 1, unpadded, one MFMA k-step
+            // (up to five with at most 32 output channels)
             l.pw_ok = dt != DT_F32 && ld.op == PPIPE_OP_CONV && l.KH * l.KW == 1 &&
-                      l.gstride == 1 && l.gpad == 0 && !l.pad_in && x.c <= 32;
+                      l.gstride == 1 && l.gpad == 0 && !l.pad_in &&
+                      (x.c <= 32 || (x.c <= 160 && o.c <= 32));
             // stem kernel: an image of at most 4 channels (below one vector), <= 52 taps
             l.stem_ok = ld.op == PPIPE_OP_CONV && l.pad_in && x.c <= 4 && l.KH * l.KW <= 52;
             if (l.tapv && l.Kpad / epv > GEMM_VTAB_MAX)

@@ -64,6 +64,10 @@ PW_CASES = [
     (24, 36, 5, 5, 2, True, "none"),
     (16, 200, 4, 4, 1, False, "relu"),
     (32, 388, 3, 9, 3, False, "relu"),
+    (96, 24, 9, 7, 3, False, "none"),       # several k-steps, at most 32 outputs
+    (144, 24, 6, 7, 2, True, "none"),
+    (160, 32, 5, 5, 2, False, "relu6"),
+    (40, 20, 7, 3, 2, True, "relu"),
 ]
 
 
