@@ -145,6 +145,122 @@ def cpu_baseline(wl, m, P, target_s):
                       f"{el:.1f} s wall"}
 
 
+def library_baseline(wl, m, P, x_nchw, steps, warmup, ref_out=None):
+    """The same partition on PyTorch-ROCm's own kernels (MIOpen convolutions,
+    BLAS linear layers, PyTorch's pooling and elementwise kernels): NHWC
+    (channels_last) activations in the workload's dtype, batch norm folded
+    into the convolution weights and bias in fp64 before the cast, the
+    residual add and activation as separate elementwise ops, softmax in fp32.
+    Timed eagerly and as one captured CUDA graph, inputs resident on the GPU.
+    A measured comparison on the same hardware, not part of the path."""
+    import numpy as np
+    import torch
+    import torch.nn.functional as F
+    torch.backends.cudnn.benchmark = True
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[wl.dtype]
+    cl = torch.channels_last
+    layers = m.layers
+    prm = {}
+    for i in range(wl.begin, wl.end):
+        L, p = layers[i], P[i]
+        if L.op not in ("conv", "fc", "fc_softmax"):
+            continue
+        w = torch.from_numpy(p["weight"]).double()
+        b = torch.from_numpy(p["bias"]).double() if "bias" in p else torch.zeros(L.c_out, dtype=torch.float64)
+        if L.bn:
+            sc = torch.from_numpy(p["bn_gamma"]).double() / torch.sqrt(
+                torch.from_numpy(p["bn_var"]).double() + 1e-5)
+            w = w * sc.reshape(-1, *([1] * (w.dim() - 1)))
+            b = (b - torch.from_numpy(p["bn_mean"]).double()) * sc + torch.from_numpy(p["bn_beta"]).double()
+        w = w.to(tdt).cuda()
+        prm[i] = (w.contiguous(memory_format=cl) if w.dim() == 4 else w, b.to(tdt).cuda())
+
+    def act(y, a):
+        if a == "relu":
+            return F.relu(y)
+        if a == "relu6":
+            return F.hardtanh(y, 0.0, 6.0)
+        return y
+
+    def fwd(x, progress=False):
+        outs = {wl.begin - 1: x}
+        last = time.perf_counter()
+        for i in range(wl.begin, wl.end):
+            if progress and time.perf_counter() - last > 10:
+                torch.cuda.synchronize()
+                print(f"[bench] library baseline first pass at layer {i}", file=sys.stderr,
+                      flush=True)
+                last = time.perf_counter()
+            L = layers[i]
+            h = outs[L.src]
+            if L.op == "conv":
+                y = F.conv2d(h, prm[i][0], prm[i][1], L.stride, L.pad, 1, L.groups)
+                if L.res_src >= 0:
+                    y = y + outs[L.res_src]
+                y = act(y, L.act)
+            elif L.op == "maxpool":
+                y = F.max_pool2d(h, L.k, L.stride, L.pad)
+            elif L.op == "gap":
+                y = h.mean((2, 3), keepdim=True)
+            else:
+                y = act(F.linear(h.flatten(1), prm[i][0], prm[i][1]), L.act)
+                if L.op == "fc_softmax":
+                    y = torch.softmax(y.float(), 1)
+            outs[i] = y
+        return outs[wl.end - 1]
+
+    x = torch.from_numpy(np.ascontiguousarray(x_nchw)).to(tdt).cuda().contiguous(memory_format=cl)
+    t0 = time.perf_counter()
+    with torch.no_grad():
+        y_eager = fwd(x, progress=True)
+        for _ in range(max(warmup, 3)):
+            y_eager = fwd(x)
+        torch.cuda.synchronize()
+        print(f"[bench] library baseline warmup {time.perf_counter() - t0:.1f} s",
+              file=sys.stderr, flush=True)
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            fwd(x)
+        torch.cuda.synchronize()
+        eager_s = time.perf_counter() - t0
+        res = {"kind": "pytorch-rocm " + torch.__version__ + " (MIOpen convolutions)",
+               "layout": "channels_last", "dtype": wl.dtype,
+               "eager_ms_per_step": eager_s * 1e3 / steps,
+               "eager_images_per_s": wl.batch * steps / eager_s}
+        try:
+            s = torch.cuda.Stream()
+            s.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(s):
+                for _ in range(3):
+                    fwd(x)
+            torch.cuda.current_stream().wait_stream(s)
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                y_graph = fwd(x)
+            for _ in range(warmup):
+                g.replay()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(steps):
+                g.replay()
+            torch.cuda.synchronize()
+            graph_s = time.perf_counter() - t0
+            res["graph_ms_per_step"] = graph_s * 1e3 / steps
+            res["graph_images_per_s"] = wl.batch * steps / graph_s
+            res["graph_equals_eager"] = bool(torch.equal(y_graph, y_eager))
+        except Exception as e:  # capture is best effort: report eager only
+            res["graph_error"] = f"{type(e).__name__}: {e}"[:200]
+    if ref_out is not None:
+        yr = y_eager.float()
+        if yr.dim() == 4:
+            yr = yr.permute(0, 2, 3, 1)
+        yr = yr.reshape(ref_out.shape)
+        d = (yr - ref_out.float()).abs().max().item()
+        res["max_abs_diff_vs_path"] = d
+        res["max_rel_diff_vs_path"] = d / max(ref_out.float().abs().max().item(), 1e-30)
+    return res
+
+
 def parse_batches(spec):
     if "-" in spec and "," not in spec:
         lo, hi = (int(v) for v in spec.split("-"))
@@ -492,6 +608,9 @@ def main():
                     help="batch sizes for --table: '1-64', or a comma list")
     ap.add_argument("--kernels", metavar="OUT.json", default=None,
                     help="also write every launch's timing record of the benchmark batch")
+    ap.add_argument("--library-baseline", action="store_true",
+                    help="also time the same partition on PyTorch-ROCm's own kernels "
+                         "(MIOpen convolutions) and add it to the line as library_baseline")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB mebibytes 10 times "
                          "(reference for the HBM byte counters) and exit")
@@ -614,6 +733,14 @@ def main():
     if args.cold_reps > 0:
         cold = part.profile_kernels_cold(wl.batch, reps=args.cold_reps)
         result["isolated_cold"] = cold_summary(cold, wl.dtype)
+    if args.library_baseline:
+        print("[bench] timing the PyTorch-ROCm library baseline", file=sys.stderr, flush=True)
+        part.run(wl.batch, xd.data_ptr(), out.data_ptr(), sp)
+        torch.cuda.synchronize()
+        lb = library_baseline(wl, m, P, x, min(args.steps, 500), 20, out)
+        lb["path_over_library_graph"] = (lb["graph_ms_per_step"] / result["ms_per_step"]
+                                         if "graph_ms_per_step" in lb else None)
+        result["library_baseline"] = lb
     if args.cpu_seconds > 0:
         print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         result["cpu_baseline"] = cpu_baseline(wl, m, P, args.cpu_seconds)
