@@ -1030,6 +1030,8 @@ GemmCfgInfo gemm_cfg_info(int cfg)
     case GEMM_DMA_64x64_8W_S3: return {64, 64, 8, false, 3, 8};
     case GEMM_DMA_64x64_8W_S4: return {64, 64, 8, false, 4, 8};
     case GEMM_DMA_64x64_8W_S6: return {64, 64, 8, false, 6, 8};
+    case GEMM_DMA_64x128_8W_S2: return {64, 128, 8, false, 2, 8};
+    case GEMM_DMA_64x256_8W_S2: return {64, 256, 8, false, 2, 8};
     default:            return {0, 0, 0, false};
     }
 }
@@ -1117,6 +1119,8 @@ static hipError_t launch_cfg(int cfg, int wk, bool tapv, const ConvGemmArgs& a,
     case GEMM_DMA_64x64_8W_S3: return launch_dma<T, 64, 64, 2, 4, 3>(tapv, a, s);
     case GEMM_DMA_64x64_8W_S4: return launch_dma<T, 64, 64, 2, 4, 4>(tapv, a, s);
     case GEMM_DMA_64x64_8W_S6: return launch_dma<T, 64, 64, 2, 4, 6>(tapv, a, s);
+    case GEMM_DMA_64x128_8W_S2: return launch_dma<T, 64, 128, 2, 4, 2>(tapv, a, s);
+    case GEMM_DMA_64x256_8W_S2: return launch_dma<T, 64, 256, 2, 4, 2>(tapv, a, s);
     default:            return hipErrorInvalidValue;
     }
 }

@@ -99,7 +99,9 @@ enum GemmCfg : int {
     // channels gathered per lane, weights staged in LDS.  wk = 16-channel
     // fragments per block (stem_channel_frags).
     GEMM_STEM = 18,
-    GEMM_NCFG = 19
+    GEMM_DMA_64x128_8W_S2 = 19,   // 8 waves, 32x32 per wave, 2 stages
+    GEMM_DMA_64x256_8W_S2 = 20,   // 8 waves, 32 co x 64 m per wave, 2 stages
+    GEMM_NCFG = 21
 };
 struct GemmCfgInfo {
     int bm, bn, kv;       // tile rows (co), columns (m); kv: 16-byte vectors of K per LDS stage

@@ -192,7 +192,10 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
     //    waves and four stages (two in flight), because a lone block streams
     //    every operand byte from beyond L2 and is bound by the bytes it keeps
     //    in flight; dense grids take the two-stage loop (fewest registers and
-    //    LDS, highest occupancy);
+    //    LDS, highest occupancy), on 8-wave 64x128 tiles for layers of at
+    //    most 64 output channels with at least 512 such tiles (fewer operand
+    //    bytes per FLOP: VGG-16 conv1_2 at batch 16 124 -> 108 us, ResNet-152's
+    //    7x7 stem at batch 64 116 -> 93 us);
     //  * small fp32 layers take the skinny kernel (no reduction pass).
     const bool wide = dt != PPIPE_F32 && Co >= 128;
     const int64_t t128 = tiles(GEMM_DMA_128x128_8W_S2);
@@ -222,6 +225,8 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
         }
         if (t * splits < 512)
             cfg = GEMM_DMA_64x64_8W_S4;
+        else if (splits == 1 && Co <= 64 && tiles(GEMM_DMA_64x128_8W_S2) >= 512)
+            cfg = GEMM_DMA_64x128_8W_S2;
     }
     //  * 16-bit 1x1 stride-1 layers with at most 32 input channels (or 160
     //    with at most 32 output channels) and at least 16384 output pixels

@@ -283,6 +283,8 @@ FORCED = [  # (configuration id, waves, splits): every kernel variant the planne
     ("14,0,1", "conv_gemm<", "64x64,kv8,8w,dma3"), ("14,0,2", "conv_gemm<", "64x64,kv8,8w,dma3"),
     ("15,0,1", "conv_gemm<", "64x64,kv8,8w,dma4"), ("15,0,3", "conv_gemm<", "64x64,kv8,8w,dma4"),
     ("16,0,1", "conv_gemm<", "64x64,kv8,8w,dma6"), ("16,0,2", "conv_gemm<", "64x64,kv8,8w,dma6"),
+    ("19,0,1", "conv_gemm<", "64x128,kv8,8w,dma2"), ("19,0,2", "conv_gemm<", "64x128,kv8,8w,dma2"),
+    ("20,0,1", "conv_gemm<", "64x256,kv8,8w,dma2"), ("20,0,3", "conv_gemm<", "64x256,kv8,8w,dma2"),
 ]
 FORCED_SHAPES = {  # ragged M and Co, padded 3x3 taps, a 1x1 with a K tail, an FC + softmax
     "3x3": ((64, 13, 13), [conv("c", -1, 64, 100, 3, 1, 1)], 3, "normal"),
@@ -291,6 +293,8 @@ FORCED_SHAPES = {  # ragged M and Co, padded 3x3 taps, a 1x1 with a K tail, an F
                              bias=True)], 5, "relu_normal"),
     # 3-channel stem: channels padded to one vector, per-vector taps
     "stem": ((3, 23, 23), [conv("c", -1, 3, 64, 7, 2, 3)], 2, "image"),
+    # several tiles of the large configurations in both dimensions, ragged
+    "3x3w": ((64, 21, 23), [conv("c", -1, 64, 300, 3, 1, 1, act="relu")], 2, "relu_normal"),
 }
 
 
