@@ -170,7 +170,8 @@ namespace {
 // shape, waves per tile (skinny) and tile order.  Deterministic in (M, Co, K,
 // dtype, eligibility) so that the latency table, the benchmark and the
 // parity tests exercise the same launches.
-Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool stem_ok)
+Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool stem_ok,
+                 bool split_free)
 {
     auto tiles = [&](int cfg) {
         GemmCfgInfo c = gemm_cfg_info(cfg);
@@ -187,11 +188,12 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
     //    keeps >= 12 steps, then while the grid is short of about 1.5 blocks
     //    per CU and each split keeps >= 4 steps, or up to 2 blocks per CU
     //    with >= 12 steps per split;
-    //  * sparse grids (under two 64x64 blocks, or one 8-wave 128x128 block,
-    //    per CU) take software-pipelined loops; sparse 64x64 grids use 8
-    //    waves and four stages (two in flight), because a lone block streams
-    //    every operand byte from beyond L2 and is bound by the bytes it keeps
-    //    in flight; dense grids take the two-stage loop (fewest registers and
+    //  * sparse grids (up to two 64x64 blocks, or under one 8-wave 128x128
+    //    block, per CU) take software-pipelined loops; sparse 64x64 grids use
+    //    8 waves and four stages (two in flight), because a lone block
+    //    streams every operand byte from beyond L2 and is bound by the bytes
+    //    it keeps in flight (VGG-16's 25088-input FC at batch 16, 64 tiles
+    //    split 8 ways: 45 -> 36 us); dense grids take the two-stage loop (fewest registers and
     //    LDS, highest occupancy), on 8-wave 64x128 tiles for layers of at
     //    most 64 output channels with at least 512 such tiles (fewer operand
     //    bytes per FLOP: VGG-16 conv1_2 at batch 16 124 -> 108 us, ResNet-152's
@@ -211,6 +213,16 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
                 splits *= 2;
         if (t128 * splits < 256)
             cfg = GEMM_DMA_128x128_8W_S3;
+    } else if (split_free) {
+        // the softmax kernel of an FC + softmax layer adds the partials as it
+        // loads the logits, so splitting K costs no reduction launch: eight
+        // ways (each split keeping >= 2 steps) on the 8-wave four-stage tile
+        // (MobileNetV2's classifier at batch 32 11.9 -> 8.5 us, VGG-16's at
+        // batch 16 10.7 -> 8.6 us)
+        const int k = steps(GEMM_DMA_64x64_8W_S4);
+        cfg = GEMM_DMA_64x64_8W_S4;
+        while (splits < 8 && k / (splits * 2) >= 2)
+            splits *= 2;
     } else {
         const int64_t t = tiles(cfg);
         const int k = steps(cfg);
@@ -223,7 +235,7 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
             if (!ok) break;
             splits *= 2;
         }
-        if (t * splits < 512)
+        if (t * splits <= 512)
             cfg = GEMM_DMA_64x64_8W_S4;
         else if (splits == 1 && Co <= 64 && tiles(GEMM_DMA_64x128_8W_S2) >= 512)
             cfg = GEMM_DMA_64x128_8W_S2;
@@ -851,7 +863,8 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
         l.plans.resize(P->max_batch);
         for (int b = 1; b <= P->max_batch; ++b) {
             const int M = b * l.Ho * l.Wo;
-            const Plan p = choose_plan(M, l.Co, l.K, dt, l.skinny_ok, l.pw_ok, l.stem_ok);
+            const Plan p = choose_plan(M, l.Co, l.K, dt, l.skinny_ok, l.pw_ok, l.stem_ok,
+                                       l.softmax);
             l.plans[b - 1] = p;
             size_t need = 0;
             if (p.splits > 1) need += (size_t)p.splits * M * l.Co;
