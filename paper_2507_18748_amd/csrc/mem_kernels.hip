@@ -9,6 +9,9 @@
 // served by L1/L2; HBM sees each input byte about once.
 #include "kernels.h"
 
+#include <cstdlib>
+#include <type_traits>
+
 namespace ppipe {
 
 template <typename T> struct Vec16 {  // 16-bit element types: 8 per vector
@@ -56,6 +59,9 @@ __device__ __forceinline__ float act_f(float v, int act)
 // 3x3 depthwise, stride S: each thread owns one 16-byte channel vector of PW
 // consecutive output pixels of one row, so an input column is loaded once for
 // every output that uses it and the nine weight vectors once per PW outputs.
+// 16-bit types multiply packed: one v_dot2 per output element and tap takes
+// the activation word as loaded (two channels) and a weight word with the
+// other channel's half zeroed, so activations are never unpacked.
 // All loads are buffer loads issued without branches: taps outside the image
 // use an offset beyond the buffer and read zeros.  Consecutive lanes take
 // consecutive channel vectors (coalesced 16-byte accesses).
@@ -92,6 +98,24 @@ __device__ __forceinline__ void unpack16(const uint4& u, float* f)
 #pragma unroll
         for (int i = 0; i < 8; ++i) f[i] = (float)e[i];
     }
+}
+
+// acc + the product of the low (HI = false) or high 16-bit element of two
+// packed pairs, with the other element's weight zero: one v_dot2 instruction
+// in place of an unpack and an FMA.  The product of two 16-bit values is
+// exact in fp32 and the zero term adds nothing, so this rounds once, as an
+// FMA does.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+template <typename T>
+__device__ __forceinline__ float dot2_acc(uint32_t x, uint32_t w, float acc)
+{
+    if constexpr (std::is_same<T, __bf16>::value)
+        return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, x),
+                                               __builtin_bit_cast(bf16x2_t, w), acc, false);
+    else
+        return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2_t, x),
+                                      __builtin_bit_cast(f16x2_t, w), acc, false);
 }
 
 template <typename T, int S, int PW>
@@ -132,28 +156,57 @@ dwconv3_kernel(const T* __restrict__ x, const T* __restrict__ w, const float* __
         for (int i = 0; i < V; ++i) acc[p][i] = 0.0f;
 
     const int wi0 = wo0 * S - pad;
+    // byte offset of tap (kh, j) = base + kh * rstride + j * cstride (32-bit
+    // wrap-around arithmetic; taps outside the image take OOB instead)
+    const uint32_t cstride = (uint32_t)C * ESZ, rstride = (uint32_t)W * cstride;
+    const uint32_t base = (uint32_t)((n * H + ho * S - pad) * W + wi0) * cstride + (uint32_t)c * ESZ;
+    uint32_t colok = 0;   // bit j: input column wi0 + j inside the image
+#pragma unroll
+    for (int j = 0; j < NCOL; ++j)
+        colok |= ((unsigned)(wi0 + j) < (unsigned)W ? 1u : 0u) << j;
 #pragma unroll
     for (int kh = 0; kh < 3; ++kh) {
         const int hi = ho * S - pad + kh;
         const bool hok = (unsigned)hi < (unsigned)H;
-        const uint32_t row = (uint32_t)(((n * H + hi) * W) * C + c) * ESZ;
+        const uint32_t row = base + (uint32_t)kh * rstride;
         uint4 xc[NCOL];
 #pragma unroll
         for (int j = 0; j < NCOL; ++j) {
-            const int wi = wi0 + j;
-            const bool ok = hok && (unsigned)wi < (unsigned)W;
-            xc[j] = dw_load(xr, ok ? row + (uint32_t)(wi * C * ESZ) : OOB);
+            const bool ok = hok && ((colok >> j) & 1u);
+            xc[j] = dw_load(xr, ok ? row + (uint32_t)j * cstride : OOB);
         }
 #pragma unroll
         for (int kw = 0; kw < 3; ++kw) {
-            float wf[V];
-            unpack16<T>(wk[kh * 3 + kw], wf);
+            if constexpr (sizeof(T) == 2) {
+                // word k of a vector holds channels 2k (low half) and 2k + 1
+                const uint4 wv = wk[kh * 3 + kw];
+                const uint32_t ww[4] = {wv.x, wv.y, wv.z, wv.w};
+                uint32_t wlo[4], whi[4];
 #pragma unroll
-            for (int p = 0; p < PW; ++p) {
-                float xf[V];
-                unpack16<T>(xc[p * S + kw], xf);
+                for (int k = 0; k < 4; ++k) {
+                    wlo[k] = ww[k] & 0x0000ffffu;
+                    whi[k] = ww[k] & 0xffff0000u;
+                }
 #pragma unroll
-                for (int i = 0; i < V; ++i) acc[p][i] = fmaf(xf[i], wf[i], acc[p][i]);
+                for (int p = 0; p < PW; ++p) {
+                    const uint4 xv = xc[p * S + kw];
+                    const uint32_t xw[4] = {xv.x, xv.y, xv.z, xv.w};
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        acc[p][2 * k] = dot2_acc<T>(xw[k], wlo[k], acc[p][2 * k]);
+                        acc[p][2 * k + 1] = dot2_acc<T>(xw[k], whi[k], acc[p][2 * k + 1]);
+                    }
+                }
+            } else {
+                float wf[V];
+                unpack16<T>(wk[kh * 3 + kw], wf);
+#pragma unroll
+                for (int p = 0; p < PW; ++p) {
+                    float xf[V];
+                    unpack16<T>(xc[p * S + kw], xf);
+#pragma unroll
+                    for (int i = 0; i < V; ++i) acc[p][i] = fmaf(xf[i], wf[i], acc[p][i]);
+                }
             }
         }
     }
@@ -163,13 +216,17 @@ dwconv3_kernel(const T* __restrict__ x, const T* __restrict__ w, const float* __
         sc[i] = scale[c + i];
         bi[i] = bias[c + i];
     }
+    // the activation as one clamp: [-inf, inf], [0, inf] or [0, 6]
+    const float lo = act == ACT_NONE ? -INFINITY : 0.0f;
+    const float hi6 = act == ACT_RELU6 ? 6.0f : INFINITY;
 #pragma unroll
     for (int p = 0; p < PW; ++p) {
         if (wo0 + p >= Wo)
             break;
         float o[V];
 #pragma unroll
-        for (int i = 0; i < V; ++i) o[i] = act_f(acc[p][i] * sc[i] + bi[i], act);
+        for (int i = 0; i < V; ++i)
+            o[i] = __builtin_amdgcn_fmed3f(fmaf(acc[p][i], sc[i], bi[i]), lo, hi6);
         Vec16<T>::store(y + ((size_t)(n * Ho + ho) * Wo + wo0 + p) * C + c, o);
     }
 }
@@ -395,25 +452,27 @@ hipError_t launch_dwconv(int dt, const void* x, const void* w, const float* scal
     if (k != 3 || (stride != 1 && stride != 2))
         return hipErrorInvalidValue;
     const int cv = C / (16 / dtype_size(dt));
-    // outputs per thread along a row: 4 on wide stride-1 maps, else 2 (more
-    // threads on small maps, fewer registers: 166 against 194 VGPRs)
-    const int pw = stride == 1 && Wo >= 96 ? 4 : 2;
+    // outputs per thread along a row: 4 at stride 1, 2 at stride 2
+    // (PPIPE_DW_PW=2 or 4 overrides the stride-1 choice for tuning sweeps)
+    int pw = stride == 1 ? 4 : 2;
+    static const int pw_force = std::getenv("PPIPE_DW_PW") ? std::atoi(std::getenv("PPIPE_DW_PW")) : 0;
+    if (stride == 1 && (pw_force == 2 || pw_force == 4))
+        pw = pw_force;
     const size_t total = (size_t)N * Ho * ((Wo + pw - 1) / pw) * cv;
     if (total >= (1u << 31) || (double)N * H * W * C * dtype_size(dt) >= 2147483648.0)
         return hipErrorInvalidValue;
+#define PPIPE_DW(S_, PW_)                                                                         \
+    PPIPE_DISPATCH(dt, PPIPE_LAUNCH((dwconv3_kernel<T, S_, PW_>), dim3(blocks_for(total)),        \
+                                    dim3(256), 0, s, (const T*)x, (const T*)w, scale, bias,       \
+                                    (T*)y, N, H, W, C, Ho, Wo, pad, act))
     if (stride == 1 && pw == 4) {
-        PPIPE_DISPATCH(dt, PPIPE_LAUNCH((dwconv3_kernel<T, 1, 4>), dim3(blocks_for(total)),
-                                        dim3(256), 0, s, (const T*)x, (const T*)w, scale,
-                                        bias, (T*)y, N, H, W, C, Ho, Wo, pad, act));
+        PPIPE_DW(1, 4);
     } else if (stride == 1) {
-        PPIPE_DISPATCH(dt, PPIPE_LAUNCH((dwconv3_kernel<T, 1, 2>), dim3(blocks_for(total)),
-                                        dim3(256), 0, s, (const T*)x, (const T*)w, scale,
-                                        bias, (T*)y, N, H, W, C, Ho, Wo, pad, act));
+        PPIPE_DW(1, 2);
     } else {
-        PPIPE_DISPATCH(dt, PPIPE_LAUNCH((dwconv3_kernel<T, 2, 2>), dim3(blocks_for(total)),
-                                        dim3(256), 0, s, (const T*)x, (const T*)w, scale,
-                                        bias, (T*)y, N, H, W, C, Ho, Wo, pad, act));
+        PPIPE_DW(2, 2);
     }
+#undef PPIPE_DW
     return hipGetLastError();
 }
 
