@@ -70,11 +70,12 @@ template <> struct Mfma<float> {
     }
 };
 
+// The activation as one clamp (v_med3_f32): [-inf, inf], [0, inf] or [0, 6].
 __device__ __forceinline__ float apply_act(float v, int act)
 {
-    if (act == ACT_RELU) return fmaxf(v, 0.0f);
-    if (act == ACT_RELU6) return fminf(fmaxf(v, 0.0f), 6.0f);
-    return v;
+    const float lo = act == ACT_NONE ? -INFINITY : 0.0f;
+    const float hi = act == ACT_RELU6 ? 6.0f : INFINITY;
+    return __builtin_amdgcn_fmed3f(v, lo, hi);
 }
 
 // Load / store 4 consecutive elements of T as one vector access.

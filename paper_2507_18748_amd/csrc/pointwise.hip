@@ -77,11 +77,12 @@ __device__ __forceinline__ uint4 pw_load16(__amdgpu_buffer_rsrc_t r, uint32_t of
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
 
+// The activation as one clamp (v_med3_f32): [-inf, inf], [0, inf] or [0, 6].
 __device__ __forceinline__ float pw_act(float v, int act)
 {
-    if (act == ACT_RELU) return fmaxf(v, 0.0f);
-    if (act == ACT_RELU6) return fminf(fmaxf(v, 0.0f), 6.0f);
-    return v;
+    const float lo = act == ACT_NONE ? -INFINITY : 0.0f;
+    const float hi = act == ACT_RELU6 ? 6.0f : INFINITY;
+    return __builtin_amdgcn_fmed3f(v, lo, hi);
 }
 
 // Epilogue of four consecutive output channels co.. (c.. within the block's
