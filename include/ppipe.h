@@ -110,7 +110,9 @@ typedef struct {
     double flops_b1;                 /* algorithmic FLOPs at batch 1 (2 per multiply-add) */
     double act_bytes_b1;             /* input + output (+ residual) activation bytes at batch 1 */
     double param_bytes;              /* weight bytes in dtype + fp32 scale/bias, once per run */
-    char kernel[96];                 /* kernel configuration chosen at the queried batch */
+    char kernel[96];                 /* kernel configuration chosen at the queried batch;
+                                        ends in " paired=J" when the layer runs in one
+                                        launch with layer J */
 } ppipe_layer_info_t;
 
 typedef struct {
@@ -141,7 +143,11 @@ ppipe_partition* ppipe_partition_create(const ppipe_model_desc* desc,
  * stream: a hipStream_t (NULL = default stream).  Asynchronous: enqueues work
  * on the stream and returns; no host synchronisation, no allocation.  If a
  * graph for (batch, in, out) was captured with ppipe_partition_capture it is
- * replayed, otherwise the kernels are launched directly.  Concurrent runs of
+ * replayed, otherwise the kernels are launched directly.  A GEMM layer and
+ * a later GEMM layer that read the same tensor (a residual stage's first
+ * convolution and its downsample projection) go out as one launch when both
+ * are planned on the same tile configuration without a K split; timed and
+ * profiled runs keep one launch sequence per layer.  Concurrent runs of
  * one handle on different streams race on its buffers. */
 int ppipe_partition_run(ppipe_partition* h, int32_t batch, const void* in,
                         void* out, void* stream);

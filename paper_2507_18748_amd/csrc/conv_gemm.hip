@@ -238,10 +238,11 @@ __device__ __forceinline__ void epi_rows(const ConvGemmArgs& a, const float* ep,
 
 // Tile index -> (m tile, co tile) after spreading the 1-D grid over the XCDs
 // in contiguous ranges (the hardware deals block b to XCD b % 8).
-__device__ __forceinline__ int3 tile_of_block(const ConvGemmArgs& a)
+// bid, G: the block's index among the G blocks of this problem (a paired
+// launch runs two problems in one grid).
+__device__ __forceinline__ int3 tile_of_block(const ConvGemmArgs& a, int bid, int G)
 {
-    const int G = gridDim.x;
-    const int xcd = blockIdx.x % NUM_XCD, slot = blockIdx.x / NUM_XCD;
+    const int xcd = bid % NUM_XCD, slot = bid / NUM_XCD;
     const int per = G / NUM_XCD, rem = G % NUM_XCD;
     int lin = xcd * per + min(xcd, rem) + slot;
     const int tiles = a.tiles_m * a.tiles_co;
@@ -250,6 +251,10 @@ __device__ __forceinline__ int3 tile_of_block(const ConvGemmArgs& a)
     const int fast = a.co_fastest ? a.tiles_co : a.tiles_m;
     const int q = lin / fast, r = lin - q * fast;
     return a.co_fastest ? make_int3(q, r, split) : make_int3(r, q, split);   // (m tile, co tile, split)
+}
+__device__ __forceinline__ int3 tile_of_block(const ConvGemmArgs& a)
+{
+    return tile_of_block(a, (int)blockIdx.x, (int)gridDim.x);
 }
 
 // ---- buffer loads -------------------------------------------------------
@@ -549,8 +554,7 @@ __device__ __forceinline__ void dma_wait()
 }
 
 template <typename T, int BM, int BN, int WM, int WN, int NS, bool TAPV>
-__global__ void __launch_bounds__(WM * WN * 64)
-conv_gemm_dma(ConvGemmArgs a)
+__device__ __forceinline__ void conv_gemm_dma_body(const ConvGemmArgs& a, int bid, int G)
 {
     constexpr int NW = WM * WN;
     constexpr int ESZ = (int)sizeof(T);
@@ -575,7 +579,7 @@ conv_gemm_dma(ConvGemmArgs a)
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave % WM, wn = wave / WM;
-    const int3 tt = tile_of_block(a);
+    const int3 tt = tile_of_block(a, bid, G);
     const int m0 = tt.x * BN, co0 = tt.y * BM;
     const int kc_begin = tt.z * a.chunks_per_split;
     const int kc_end = min(a.total_chunks, kc_begin + a.chunks_per_split);
@@ -784,6 +788,30 @@ conv_gemm_dma(ConvGemmArgs a)
         else
             epi_rows<T, 4, BM, LROW, NW * 64>(a, ep, rows, m0 + p0, co0, tt.z, tid);
     }
+}
+
+template <typename T, int BM, int BN, int WM, int WN, int NS, bool TAPV>
+__global__ void __launch_bounds__(WM * WN * 64)
+conv_gemm_dma(ConvGemmArgs a)
+{
+    conv_gemm_dma_body<T, BM, BN, WM, WN, NS, TAPV>(a, (int)blockIdx.x, (int)gridDim.x);
+}
+
+// Two independent layers of one tile configuration in one launch: blocks
+// [0, n0) compute problem 0, the rest problem 1 (a residual block's first
+// convolution and its downsample projection, which read the same input).
+struct ConvGemmPair {
+    ConvGemmArgs a[2];
+    int n0;
+};
+template <typename T, int BM, int BN, int WM, int WN, int NS>
+__global__ void __launch_bounds__(WM * WN * 64)
+conv_gemm_dma_pair(ConvGemmPair p)
+{
+    const int bid = (int)blockIdx.x;
+    const int q = bid < p.n0 ? 0 : 1;   // block-uniform: one inlined body
+    conv_gemm_dma_body<T, BM, BN, WM, WN, NS, false>(p.a[q], q ? bid - p.n0 : bid,
+                                                      q ? (int)gridDim.x - p.n0 : p.n0);
 }
 
 // Split-K reduction: one thread per 4 output channels of one pixel, partials
@@ -1067,6 +1095,25 @@ static hipError_t launch_dma_one(const ConvGemmArgs& a, hipStream_t s)
 }
 
 template <typename T, int BM, int BN, int WM, int WN, int NS>
+static hipError_t launch_dma_pair(const ConvGemmArgs& a0, const ConvGemmArgs& a1, hipStream_t s)
+{
+    constexpr int bytes = NS * (BM + BN) * 128;
+    static const hipError_t attr = hipFuncSetAttribute(
+        (const void*)conv_gemm_dma_pair<T, BM, BN, WM, WN, NS>,
+        hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (attr != hipSuccess)
+        return attr;
+    ConvGemmPair p;
+    p.a[0] = a0;
+    p.a[1] = a1;
+    p.n0 = a0.tiles_m * a0.tiles_co * a0.splits;
+    const int n1 = a1.tiles_m * a1.tiles_co * a1.splits;
+    PPIPE_LAUNCH((conv_gemm_dma_pair<T, BM, BN, WM, WN, NS>), dim3((unsigned)(p.n0 + n1)),
+                 dim3(WM * WN * 64), bytes, s, p);
+    return hipGetLastError();
+}
+
+template <typename T, int BM, int BN, int WM, int WN, int NS>
 static hipError_t launch_dma(bool tapv, const ConvGemmArgs& a, hipStream_t s)
 {
     return tapv ? launch_dma_one<T, BM, BN, WM, WN, NS, true>(a, s)
@@ -1123,6 +1170,39 @@ static hipError_t launch_cfg(int cfg, int wk, bool tapv, const ConvGemmArgs& a,
     case GEMM_DMA_64x128_8W_S2: return launch_dma<T, 64, 128, 2, 4, 2>(tapv, a, s);
     case GEMM_DMA_64x256_8W_S2: return launch_dma<T, 64, 256, 2, 4, 2>(tapv, a, s);
     default:            return hipErrorInvalidValue;
+    }
+}
+
+template <typename T>
+static hipError_t launch_pair_cfg(int cfg, const ConvGemmArgs& a0, const ConvGemmArgs& a1,
+                                  hipStream_t s)
+{
+    switch (cfg) {
+    case GEMM_DMA_64x64_S2: return launch_dma_pair<T, 64, 64, 2, 2, 2>(a0, a1, s);
+    case GEMM_DMA_64x64_S3: return launch_dma_pair<T, 64, 64, 2, 2, 3>(a0, a1, s);
+    case GEMM_DMA_128x128_8W_S2: return launch_dma_pair<T, 128, 128, 2, 4, 2>(a0, a1, s);
+    case GEMM_DMA_128x128_8W_S3: return launch_dma_pair<T, 128, 128, 2, 4, 3>(a0, a1, s);
+    case GEMM_DMA_64x64_8W_S2: return launch_dma_pair<T, 64, 64, 2, 4, 2>(a0, a1, s);
+    case GEMM_DMA_64x64_8W_S3: return launch_dma_pair<T, 64, 64, 2, 4, 3>(a0, a1, s);
+    case GEMM_DMA_64x64_8W_S4: return launch_dma_pair<T, 64, 64, 2, 4, 4>(a0, a1, s);
+    case GEMM_DMA_64x64_8W_S6: return launch_dma_pair<T, 64, 64, 2, 4, 6>(a0, a1, s);
+    case GEMM_DMA_64x128_8W_S2: return launch_dma_pair<T, 64, 128, 2, 4, 2>(a0, a1, s);
+    case GEMM_DMA_64x256_8W_S2: return launch_dma_pair<T, 64, 256, 2, 4, 2>(a0, a1, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_conv_gemm_pair(int dt, int cfg, const ConvGemmArgs& a0, const ConvGemmArgs& a1,
+                                 hipStream_t s)
+{
+    if (gemm_cfg_info(cfg).dma == 0 || a0.splits != 1 || a1.splits != 1 || a0.softmax ||
+        a1.softmax)
+        return hipErrorInvalidValue;
+    switch (dt) {
+    case DT_F32:  return launch_pair_cfg<float>(cfg, a0, a1, s);
+    case DT_F16:  return launch_pair_cfg<_Float16>(cfg, a0, a1, s);
+    case DT_BF16: return launch_pair_cfg<__bf16>(cfg, a0, a1, s);
+    default:      return hipErrorInvalidValue;
     }
 }
 

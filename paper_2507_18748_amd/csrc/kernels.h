@@ -127,6 +127,12 @@ constexpr int SKINNY_MAX_WAVES = 16;
 // table (channel count a multiple of the vector width but not of the stage).
 hipError_t launch_conv_gemm(int dt, int cfg, int wk, bool tapv, const ConvGemmArgs& a,
                             hipStream_t s);
+// Two layers of one DMA tile configuration, each unsplit and without a
+// softmax, in one launch (blocks of a0 first, then of a1).  The layers must
+// not depend on each other; both take plain per-tap K steps (no per-vector
+// tap table).
+hipError_t launch_conv_gemm_pair(int dt, int cfg, const ConvGemmArgs& a0, const ConvGemmArgs& a1,
+                                 hipStream_t s);
 const char* conv_gemm_name(int dt, int cfg, int wk, bool tapv);
 
 // Streaming 1x1 convolution (GEMM_PW) of a 16-bit layer with C <= 32, or

@@ -119,6 +119,10 @@ struct LayerRT {
     float* scale = nullptr;
     float* bias = nullptr;
     int in_buf = BUF_IN, res_buf = BUF_NONE, out_buf = BUF_OUT;
+    // position in the partition of the layer this GEMM shares its input with
+    // and may run with in one launch (-1: none); pair_lead on the earlier one
+    int pair = -1;
+    bool pair_lead = false;
     std::vector<Plan> plans;   // [batch - 1]
     int64_t out_bytes_b1 = 0;
     double flops_b1 = 0, in_bytes_b1 = 0, res_bytes_b1 = 0, param_bytes = 0;
@@ -411,6 +415,54 @@ void launch_work(const ppipe_partition* P, const LayerRT& l, int batch, int laun
     *bytes = by;
 }
 
+// GEMM arguments of layer l at a batch (x: the layer's input as the GEMM reads it).
+ConvGemmArgs gemm_args(const ppipe_partition* P, const LayerRT& l, int batch, const void* x,
+                       const void* res, void* y, bool padded)
+{
+    const Plan& p = l.plans[batch - 1];
+    ConvGemmArgs a;
+    a.x = x;
+    a.w = l.w;
+    a.scale = l.scale;
+    a.bias = l.bias;
+    a.res = res;
+    a.y = y;
+    a.M = batch * l.Ho * l.Wo;
+    a.partial = P->ws;
+    a.logits = P->ws + (p.splits > 1 ? (size_t)p.splits * a.M * l.Co : 0);
+    a.N = batch;
+    a.H = l.H; a.W = l.W; a.C = padded ? l.cpad : l.C;
+    a.Ho = l.Ho; a.Wo = l.Wo; a.Co = l.Co;
+    a.KH = l.KH; a.KW = l.KW; a.stride = l.gstride; a.pad = l.gpad;
+    a.K = l.K; a.Kpad = l.Kpad;
+    a.act = l.act;
+    a.total_chunks = p.total_chunks;
+    a.splits = p.splits;
+    a.chunks_per_split = p.chunks_per_split;
+    a.tiles_m = p.tiles_m;
+    a.tiles_co = p.tiles_co;
+    a.co_fastest = p.co_fastest;
+    a.softmax = l.softmax ? 1 : 0;
+    a.grid_blocks = p.grid;
+    return a;
+}
+
+// Whether paired layers a (lead) and b run as one launch at this batch: both
+// planned unsplit on the sparse-grid configuration (8-wave 64x64, four
+// stages), where neither grid fills the chip and each launch is bound by its
+// latency.  Dense grids gain nothing from sharing a launch (ResNet-152 at
+// batch 16 ran 0.7% slower with its two dense pairs joined).  PPIPE_NO_PAIR
+// turns pairing off (A/B timing).
+bool pair_runs(const LayerRT& a, const LayerRT& b, int batch)
+{
+    static const bool off = std::getenv("PPIPE_NO_PAIR") != nullptr;
+    const Plan& p = a.plans[batch - 1];
+    const Plan& q = b.plans[batch - 1];
+    return !off && p.cfg == GEMM_DMA_64x64_8W_S4 && q.cfg == GEMM_DMA_64x64_8W_S4 &&
+           p.splits == 1 && q.splits == 1 && !pads_input(a, p) && !pads_input(b, q) &&
+           !tapv_of(a, p) && !tapv_of(b, q);
+}
+
 // Enqueue the launches of one layer; only >= 0 restricts to that launch.
 hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, const void* in,
                          void* out, hipStream_t s, LaunchHook* hook, int only = -1)
@@ -436,30 +488,8 @@ hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, 
             }
             ++li;
         }
-        ConvGemmArgs a;
-        a.x = pad ? (const void*)P->pad_buf : x;
-        a.w = l.w;
-        a.scale = l.scale;
-        a.bias = l.bias;
-        a.res = res;
-        a.y = y;
-        a.M = batch * l.Ho * l.Wo;
-        a.partial = P->ws;
-        a.logits = P->ws + (p.splits > 1 ? (size_t)p.splits * a.M * l.Co : 0);
-        a.N = batch;
-        a.H = l.H; a.W = l.W; a.C = pad ? l.cpad : l.C;
-        a.Ho = l.Ho; a.Wo = l.Wo; a.Co = l.Co;
-        a.KH = l.KH; a.KW = l.KW; a.stride = l.gstride; a.pad = l.gpad;
-        a.K = l.K; a.Kpad = l.Kpad;
-        a.act = l.act;
-        a.total_chunks = p.total_chunks;
-        a.splits = p.splits;
-        a.chunks_per_split = p.chunks_per_split;
-        a.tiles_m = p.tiles_m;
-        a.tiles_co = p.tiles_co;
-        a.co_fastest = p.co_fastest;
-        a.softmax = l.softmax ? 1 : 0;
-        a.grid_blocks = p.grid;
+        const ConvGemmArgs a =
+            gemm_args(P, l, batch, pad ? (const void*)P->pad_buf : x, res, y, pad);
         if (want(li)) {
             if (hook) hook->before(l, li, s);
             e = launch_conv_gemm(P->dtype, p.cfg, p.wk, tapv_of(l, p), a, s);
@@ -507,11 +537,32 @@ hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, 
     }
 }
 
+// The whole range in layer order.  Without a hook (the run and capture
+// paths), paired layers whose plans allow it go out as one launch at the
+// lead's position; runs with a hook (per-layer and per-launch timing) keep
+// one launch sequence per layer.
 hipError_t enqueue_all(const ppipe_partition* P, int batch, const void* in, void* out,
                        hipStream_t s, LaunchHook* hook)
 {
     for (const LayerRT& l : P->L) {
-        hipError_t e = enqueue_layer(P, l, batch, in, out, s, hook);
+        hipError_t e;
+        if (!hook && l.pair >= 0 && pair_runs(l.pair_lead ? l : P->L[l.pair],
+                                              l.pair_lead ? P->L[l.pair] : l, batch)) {
+            if (!l.pair_lead)
+                continue;   // ran with its lead
+            const LayerRT& m = P->L[l.pair];
+            const ConvGemmArgs a0 = gemm_args(P, l, batch, buf_ptr(P, l.in_buf, in, out),
+                                              buf_ptr(P, l.res_buf, in, out),
+                                              const_cast<void*>(buf_ptr(P, l.out_buf, in, out)),
+                                              false);
+            const ConvGemmArgs a1 = gemm_args(P, m, batch, buf_ptr(P, m.in_buf, in, out),
+                                              buf_ptr(P, m.res_buf, in, out),
+                                              const_cast<void*>(buf_ptr(P, m.out_buf, in, out)),
+                                              false);
+            e = launch_conv_gemm_pair(P->dtype, l.plans[batch - 1].cfg, a0, a1, s);
+        } else {
+            e = enqueue_layer(P, l, batch, in, out, s, hook);
+        }
         if (e != hipSuccess)
             return e;
     }
@@ -820,7 +871,32 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
     }
     P->host_blob.swap(blob);
 
+    // ---- paired GEMMs ----
+    // A GEMM layer and a later GEMM layer reading the same tensor (a residual
+    // stage's first convolution and its downsample projection) may run as one
+    // launch; the later one's output is then written at the earlier one's
+    // position.  Neither may be the last layer, take the softmax or need the
+    // channel-padding pass or the per-vector tap table.
+    auto pairable = [&](const LayerRT& l, int i) {
+        return l.kind == K_GEMM && !l.softmax && !l.pad_in && !l.tapv && i < end - 1;
+    };
+    for (int i = begin; i < end; ++i) {
+        LayerRT& a = P->L[i - begin];
+        if (a.pair >= 0 || !pairable(a, i)) continue;
+        for (int j = i + 1; j < end; ++j) {
+            LayerRT& b = P->L[j - begin];
+            if (b.pair < 0 && pairable(b, j) && d->layers[j].src == d->layers[i].src) {
+                a.pair = j - begin;
+                a.pair_lead = true;
+                b.pair = i - begin;
+                break;
+            }
+        }
+    }
+
     // ---- activation buffers by liveness ----
+    // A paired layer's output slot is taken at its lead's position, so that
+    // it is reserved whichever order the two run in.
     std::vector<int> last_use(end - begin, -1);
     for (int i = begin; i < end; ++i) {
         const ppipe_layer_desc& ld = d->layers[i];
@@ -828,20 +904,11 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
             if (r >= begin) last_use[r - begin] = std::max(last_use[r - begin], i);
     }
     std::vector<int> slot_busy_until;
-    for (int i = begin; i < end; ++i) {
-        LayerRT& l = P->L[i - begin];
-        const ppipe_layer_desc& ld = d->layers[i];
-        l.in_buf = ld.src >= begin ? P->L[ld.src - begin].out_buf : BUF_IN;
-        l.res_buf = ld.res_src == -1 ? BUF_NONE
-                    : (ld.res_src >= begin ? P->L[ld.res_src - begin].out_buf : BUF_IN);
-        if (i == end - 1) {
-            l.out_buf = BUF_OUT;
-            break;
-        }
+    auto take_slot = [&](LayerRT& l, int i, int at) {
         const size_t need = (size_t)P->max_batch * (size_t)l.out_bytes_b1;
         int slot = -1;
         for (size_t s = 0; s < slot_busy_until.size(); ++s)
-            if (slot_busy_until[s] < i) {
+            if (slot_busy_until[s] < at) {
                 // prefer a free slot that is already large enough
                 if (slot < 0 || (P->slot_bytes[s] >= need && P->slot_bytes[slot] < need))
                     slot = (int)s;
@@ -854,6 +921,22 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
         slot_busy_until[slot] = std::max(last_use[i - begin], i);
         P->slot_bytes[slot] = std::max(P->slot_bytes[slot], need);
         l.out_buf = slot;
+    };
+    for (int i = begin; i < end; ++i) {
+        LayerRT& l = P->L[i - begin];
+        const ppipe_layer_desc& ld = d->layers[i];
+        l.in_buf = ld.src >= begin ? P->L[ld.src - begin].out_buf : BUF_IN;
+        l.res_buf = ld.res_src == -1 ? BUF_NONE
+                    : (ld.res_src >= begin ? P->L[ld.res_src - begin].out_buf : BUF_IN);
+        if (i == end - 1) {
+            l.out_buf = BUF_OUT;
+            break;
+        }
+        if (l.pair >= 0 && !l.pair_lead)
+            continue;                        // slot taken with its lead
+        take_slot(l, i, i);
+        if (l.pair_lead)
+            take_slot(P->L[l.pair], begin + l.pair, i);
     }
 
     // ---- kernel plans for every batch, logits workspace ----
@@ -1519,6 +1602,9 @@ int ppipe_layer_info(const ppipe_partition* h, int32_t index, int32_t batch,
         const Plan& p = l.plans[batch - 1];
         k += " tiles=" + std::to_string(p.tiles_m * p.tiles_co) + " splits=" +
              std::to_string(p.splits);
+        if (l.pair >= 0 && pair_runs(l.pair_lead ? l : h->L[l.pair],
+                                     l.pair_lead ? h->L[l.pair] : l, batch))
+            k += " paired=" + std::to_string(h->L[l.pair].index);
     }
     std::snprintf(info->kernel, sizeof(info->kernel), "%s", k.c_str());
     return PPIPE_OK;

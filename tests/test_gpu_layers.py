@@ -316,3 +316,65 @@ def test_forced_gemm_configuration(monkeypatch, plan, family, tile, shape, dtype
     assert k.startswith(family) and tile in k, (plan, k)
     tol = {"f32": 1e-5, "bf16": 2.0 ** -7}[dtype] if shape != "fc" else 2e-2
     check(m, dtype, batch, kind=kind, tol=tol)
+
+
+# A residual stage's first bottleneck: conv1 and the downsample projection read
+# the stage input and go out as one launch when their plans match.
+def _bottleneck(ci, mid, co, hw, s):
+    return make((ci, hw, hw), [
+        conv("conv1", -1, ci, mid),
+        conv("conv2", 0, mid, mid, 3, s, 1),
+        conv("down", -1, ci, co, 1, s, 0, act="none"),
+        conv("conv3", 1, mid, co, act="relu", res=2),
+        dict(name="pool", op="gap", src=3, c_in=co, c_out=co),
+    ])
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("ci,mid,co,hw,s,batch", [
+    (256, 128, 512, 14, 2, 4),     # ResNet-50 layer2-like stage entry, two tiles of each
+    (64, 64, 256, 9, 1, 3),        # stride 1 (ResNet layer1), ragged tiles
+    (512, 256, 1024, 7, 2, 8),
+])
+def test_paired_downsample_launch(dtype, ci, mid, co, hw, s, batch):
+    """conv1 and the downsample run as one launch (the layer info says so),
+    match the oracle, and equal the per-layer launch sequence of a timed run
+    bit for bit, directly and from a captured graph replayed twice."""
+    import torch
+    from paper_2507_18748_amd import Partition
+    from gpu_util import upload_nhwc, empty_out
+    m = _bottleneck(ci, mid, co, hw, s)
+    P = W.model_params(m, 3, dtype)
+    x = W.partition_input((ci, hw, hw), batch, 3, dtype, "relu_normal")
+    print(f"[paired] {ci},{mid},{co} hw={hw} s={s} dtype={dtype} batch={batch}", flush=True)
+    ref = oracle.forward(m.layers, P, 0, len(m.layers), x, dtype)
+    with Partition(m.layers, P, (ci, hw, hw), 0, len(m.layers), dtype, max_batch=batch) as part:
+        k0 = part.layer_info(0, batch)["kernel"]
+        k2 = part.layer_info(2, batch)["kernel"]
+        paired = "paired=2" in k0
+        assert paired == ("paired=0" in k2), (k0, k2)
+        xd = upload_nhwc(x, dtype)
+        outs = []
+        for mode in ("timed", "direct", "graph"):
+            out = empty_out(part, batch)
+            out.fill_(float("nan"))
+            st = torch.cuda.current_stream().cuda_stream
+            if mode == "timed":
+                part.timing_setup(batch, xd.data_ptr(), out.data_ptr())
+                part.run_timed(st)
+                part.timing_read()
+            elif mode == "direct":
+                part.run(batch, xd.data_ptr(), out.data_ptr(), st)
+            else:
+                part.capture(batch, xd.data_ptr(), out.data_ptr())
+                for _ in range(2):
+                    part.run(batch, xd.data_ptr(), out.data_ptr(), st)
+                    torch.cuda.synchronize()
+            torch.cuda.synchronize()
+            outs.append(out.float().cpu().numpy().copy())
+    for o in outs[1:]:
+        np.testing.assert_array_equal(o, outs[0])
+    got = outs[0].reshape(ref.shape)
+    assert rel_inf(got, ref) <= LAYER_TOL[dtype]
+    if dtype != "f32":
+        assert paired, (k0, k2)
