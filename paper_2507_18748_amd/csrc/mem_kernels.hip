@@ -269,6 +269,59 @@ maxpool_kernel(const T* __restrict__ x, T* __restrict__ y, int N, int H, int W, 
     Vec16<T>::store(y + (((size_t)n * Ho + ho) * Wo + wo) * C + c, m);
 }
 
+// Max pooling with a fixed K x K window and stride S: the K*K tap loads are
+// buffer loads issued together, without branches (taps outside the image
+// load at an offset past the buffer and are then replaced by -inf), so a
+// thread's loads are in flight at once instead of one loop trip at a time.
+template <typename T, int K, int S>
+__global__ void __launch_bounds__(256)
+maxpool_fixed_kernel(const T* __restrict__ x, T* __restrict__ y, int N, int H, int W, int C,
+                     int Ho, int Wo, int pad)
+{
+    constexpr int V = Vec16<T>::N;
+    constexpr int ESZ = (int)sizeof(T);
+    constexpr uint32_t OOB = 0x80000000u;
+    const int CV = C / V;
+    const uint32_t total = (uint32_t)N * Ho * Wo * CV;
+    const uint32_t idx = xcd_block() * 256u + threadIdx.x;
+    if (idx >= total)
+        return;
+    const int cv = (int)(idx % CV);
+    uint32_t t = idx / CV;
+    const int wo = (int)(t % Wo);
+    t /= Wo;
+    const int ho = (int)(t % Ho);
+    const int n = (int)(t / Ho);
+    const int c = cv * V;
+    const auto xr = dw_rsrc(x, (uint32_t)N * H * W * C * ESZ);
+    const uint32_t cstride = (uint32_t)C * ESZ, rstride = (uint32_t)W * cstride;
+    const int hi0 = ho * S - pad, wi0 = wo * S - pad;
+    const uint32_t base = (uint32_t)((n * H + hi0) * W + wi0) * cstride + (uint32_t)c * ESZ;
+    uint4 v[K * K];
+    uint32_t okm = 0;   // bit kh * K + kw: the tap is inside the image
+#pragma unroll
+    for (int kh = 0; kh < K; ++kh)
+#pragma unroll
+        for (int kw = 0; kw < K; ++kw) {
+            const bool ok = (unsigned)(hi0 + kh) < (unsigned)H && (unsigned)(wi0 + kw) < (unsigned)W;
+            okm |= (ok ? 1u : 0u) << (kh * K + kw);
+            v[kh * K + kw] = dw_load(xr, ok ? base + (uint32_t)kh * rstride + (uint32_t)kw * cstride
+                                            : OOB);
+        }
+    float m[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i) m[i] = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < K * K; ++q) {
+        float f[V];
+        unpack16<T>(v[q], f);
+        const bool ok = (okm >> q) & 1u;
+#pragma unroll
+        for (int i = 0; i < V; ++i) m[i] = fmaxf(m[i], ok ? f[i] : -INFINITY);
+    }
+    Vec16<T>::store(y + ((size_t)(n * Ho + ho) * Wo + wo) * C + c, m);
+}
+
 // Global average pool: a block owns 16 channel vectors (128 or 64 channels)
 // of one image; its 16 thread rows split the H*W pixels (every 16th pixel per
 // thread, loads issued four at a time), so every pixel row of the block is
@@ -480,9 +533,20 @@ hipError_t launch_maxpool(int dt, const void* x, void* y, int N, int H, int W, i
                           int Ho, int Wo, int k, int stride, int pad, hipStream_t s)
 {
     const size_t total = (size_t)N * Ho * Wo * C / (16 / dtype_size(dt));
-    PPIPE_DISPATCH(dt, PPIPE_LAUNCH(maxpool_kernel<T>, dim3(blocks_for(total)),
-                                          dim3(256), 0, s, (const T*)x, (T*)y, N, H, W, C,
-                                          Ho, Wo, k, stride, pad));
+    const bool fits32 = total < (1u << 31) && (double)N * H * W * C * dtype_size(dt) < 2147483648.0;
+    if (fits32 && k == 2 && stride == 2) {
+        PPIPE_DISPATCH(dt, PPIPE_LAUNCH((maxpool_fixed_kernel<T, 2, 2>), dim3(blocks_for(total)),
+                                        dim3(256), 0, s, (const T*)x, (T*)y, N, H, W, C, Ho, Wo,
+                                        pad));
+    } else if (fits32 && k == 3 && stride == 2) {
+        PPIPE_DISPATCH(dt, PPIPE_LAUNCH((maxpool_fixed_kernel<T, 3, 2>), dim3(blocks_for(total)),
+                                        dim3(256), 0, s, (const T*)x, (T*)y, N, H, W, C, Ho, Wo,
+                                        pad));
+    } else {
+        PPIPE_DISPATCH(dt, PPIPE_LAUNCH(maxpool_kernel<T>, dim3(blocks_for(total)),
+                                        dim3(256), 0, s, (const T*)x, (T*)y, N, H, W, C,
+                                        Ho, Wo, k, stride, pad));
+    }
     return hipGetLastError();
 }
 

@@ -187,7 +187,8 @@ def test_depthwise3x3(dtype, stride, chw):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
-@pytest.mark.parametrize("k,s,p,hw", [(3, 2, 1, 15), (2, 2, 0, 12), (3, 2, 1, 112)])
+@pytest.mark.parametrize("k,s,p,hw", [(3, 2, 1, 15), (2, 2, 0, 12), (3, 2, 1, 112),
+                                      (2, 2, 0, 13), (3, 1, 1, 9), (3, 2, 0, 14)])
 def test_maxpool_bit_exact(dtype, k, s, p, hw):
     m = make((64, hw, hw), [dict(name="pool", op="maxpool", src=-1, c_in=64, c_out=64, k=k,
                                  stride=s, pad=p)])
