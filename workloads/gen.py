@@ -7,7 +7,7 @@ which other layers are generated: input = ``[seed, 0]``, layer i =
 to the storage dtype (round to nearest even), and handed to both consumers as
 float32 arrays whose values are exactly representable in that dtype.
 
-Initialisation (no trained weights exist for this build):
+Initialisation (random, not trained weights):
   conv / fc weight  N(0, 2 / fan_in), fan_in = (c_in / groups) * k * k or in_features
   bias              N(0, 0.01^2)
   batch norm        gamma = layer.gamma, beta = 0, mean ~ N(0, 0.1^2), var ~ U(0.5, 1.5)
