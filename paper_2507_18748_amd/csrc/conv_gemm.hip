@@ -720,19 +720,27 @@ __device__ __forceinline__ void conv_gemm_dma_body(const ConvGemmArgs& a, int bi
                                    // fragments fed this wave's MFMAs)
                 issue(lds0 + ((s + 1) & 1) * STAGE);
                 const unsigned char* S = dyn_smem + (s & 1) * STAGE;
+                // Every fragment read of the stage goes out before its first
+                // MFMA, so the products of k-step 0 run while the reads of
+                // k-step 1 are in flight (left to itself the compiler reuses
+                // a few registers and waits on each read in turn).
+                uint4 af[KV / 4][FM], bf[KV / 4][FN];
 #pragma unroll
                 for (int ks = 0; ks < KV / 4; ++ks) {
-                    uint4 af[FM], bf[FN];
 #pragma unroll
-                    for (int i = 0; i < FM; ++i) af[i] = *(const uint4*)(S + (fa[i] ^ (ks * 64)));
+                    for (int i = 0; i < FM; ++i) af[ks][i] = *(const uint4*)(S + (fa[i] ^ (ks * 64)));
 #pragma unroll
-                    for (int j = 0; j < FN; ++j) bf[j] = *(const uint4*)(S + (fb[j] ^ (ks * 64)));
+                    for (int j = 0; j < FN; ++j) bf[ks][j] = *(const uint4*)(S + (fb[j] ^ (ks * 64)));
+                }
+#pragma unroll
+                for (int ks = 0; ks < KV / 4; ++ks)
 #pragma unroll
                     for (int i = 0; i < FM; ++i)
 #pragma unroll
                         for (int j = 0; j < FN; ++j)
-                            Mfma<T>::step(af[i], bf[j], acc[i][j]);
-                }
+                            Mfma<T>::step(af[ks][i], bf[ks][j], acc[i][j]);
+                __builtin_amdgcn_sched_group_barrier(0x100, (KV / 4) * (FM + FN), 0);   // LDS reads
+                __builtin_amdgcn_sched_group_barrier(0x008, (KV / 4) * FM * FN, 0);     // then MFMAs
             }
             dma_wait<0>();   // the empty tail load
         }
