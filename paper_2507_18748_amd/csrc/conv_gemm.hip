@@ -702,8 +702,12 @@ __device__ __forceinline__ void conv_gemm_dma_body(const ConvGemmArgs& a, int bi
         bare_barrier();               /* ... and every wave's; stage s - 2 is consumed */         \
         issue(lds0 + wr * STAGE);                                                                 \
         PPIPE_READ(dyn_smem + rd * STAGE, XA, XB);                                                \
-        if ((s) > 0)                                                                              \
+        if ((s) > 0) {                                                                            \
             PPIPE_MMA(YA, YB);                                                                    \
+            /* the reads of stage s all go out before the products of s - 1 */                   \
+            __builtin_amdgcn_sched_group_barrier(0x100, (KV / 4) * (FM + FN), 0);                 \
+            __builtin_amdgcn_sched_group_barrier(0x008, (KV / 4) * FM * FN, 0);                   \
+        }                                                                                         \
         rd = rd + 1 == NS ? 0 : rd + 1;                                                           \
         wr = wr + 1 == NS ? 0 : wr + 1;                                                           \
     } while (0)
