@@ -17,9 +17,13 @@
 //     buffer range check returns zeros), issued PF groups ahead;
 //   * 16 x 16 x 32 MFMAs (one per 16 output channels and k-step) give each
 //     lane four consecutive output channels of one pixel;
-//   * the epilogue (folded BN scale and shift from LDS, residual, activation,
-//     rounding) stores those four channels as one 8-byte vector, so a wave's
-//     store covers 32 contiguous bytes of each of its 16 pixel rows.
+//   * the epilogue stages the group's scaled sums (folded BN scale and shift
+//     from LDS) as a [16 pixel][channel] fp32 tile in the wave's own LDS
+//     rows; each lane then finishes one 8-channel vector of one pixel
+//     (residual, activation, rounding) and stores 16 contiguous bytes, so a
+//     wave's stores run along the pixels' channel rows (output channels a
+//     multiple of 8; otherwise each lane stores its four channels as one
+//     8-byte vector, 32-byte pieces of 16 rows per store).
 //
 // Stem (GEMM_STEM).  A k x k convolution of a C <= 4 channel image (RGB
 // stems) is bound by writing its output.  The weights are packed as for the
@@ -130,6 +134,16 @@ __global__ void __launch_bounds__(PW_WAVES * 64) pw_conv_kernel(ConvGemmArgs a)
     constexpr int PW_PF = KS == 1 ? 3 : 1;
     constexpr int ESZ = (int)sizeof(T);
     __shared__ float s_scale[CF * 16], s_bias[CF * 16];
+    // Row-contiguous stores: a wave stages its group's scaled sums as a
+    // [16 pixel][16 CF channel] fp32 tile in its own LDS rows, then every lane
+    // finishes one 8-channel vector of one pixel (residual, activation,
+    // rounding) and stores 16 contiguous bytes, so consecutive lanes write
+    // along each pixel's channel row instead of 32-byte pieces of 16 rows.
+    constexpr int NV = 2 * CF;                  // 8-channel vectors of a pixel's slice
+    constexpr int NIT = (16 * NV + 63) / 64;    // vectors per lane and group
+    constexpr int TROW = CF * 16 + 4;           // floats per staged pixel row
+    __shared__ __attribute__((aligned(16))) float s_tile[PW_WAVES][16][TROW];
+    const bool rows_out = a.Co % 8 == 0;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -188,14 +202,57 @@ __global__ void __launch_bounds__(PW_WAVES * 64) pw_conv_kernel(ConvGemmArgs a)
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) bq[d][ks] = bq[d + 1][ks];
 
-        const int p = g * 16 + (lane & 15);
-        if (p < a.M) {
+        if (rows_out) {
+            float* tw = &s_tile[wave][0][0];
 #pragma unroll
             for (int f = 0; f < CF; ++f) {
-                const int c = 16 * f + cl, co = co0 + c;
-                if (co >= a.Co)
-                    break;
-                pw_store4<T>(a, p, co, c, acc[f], s_scale, s_bias);
+                const int c = 16 * f + cl;
+                float4 v;
+                v.x = acc[f][0] * s_scale[c] + s_bias[c];
+                v.y = acc[f][1] * s_scale[c + 1] + s_bias[c + 1];
+                v.z = acc[f][2] * s_scale[c + 2] + s_bias[c + 2];
+                v.w = acc[f][3] * s_scale[c + 3] + s_bias[c + 3];
+                *(float4*)(tw + (lane & 15) * TROW + c) = v;
+            }
+            __builtin_amdgcn_wave_barrier();   // one wave's LDS operations run in order
+#pragma unroll
+            for (int it = 0; it < NIT; ++it) {
+                const int v = it * 64 + lane;
+                const int px = v / NV, cv = v - px * NV;
+                const int p = g * 16 + px, co = co0 + 8 * cv;
+                if (v < 16 * NV && p < a.M && co < a.Co) {
+                    const size_t off = (size_t)p * a.Co + co;
+                    uint4 r = make_uint4(0u, 0u, 0u, 0u);
+                    if (a.res)
+                        r = *(const uint4*)((const T*)a.res + off);
+                    const float4 lo = *(const float4*)(tw + px * TROW + 8 * cv);
+                    const float4 hi = *(const float4*)(tw + px * TROW + 8 * cv + 4);
+                    float o[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+                    if (a.res) {
+                        T rr[8];
+                        __builtin_memcpy(rr, &r, 16);
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) o[q] += (float)rr[q];
+                    }
+                    T e[8];
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) e[q] = (T)pw_act(o[q], a.act);
+                    uint4 u;
+                    __builtin_memcpy(&u, e, 16);
+                    *(uint4*)((T*)a.y + off) = u;
+                }
+            }
+            __builtin_amdgcn_wave_barrier();
+        } else {
+            const int p = g * 16 + (lane & 15);
+            if (p < a.M) {
+#pragma unroll
+                for (int f = 0; f < CF; ++f) {
+                    const int c = 16 * f + cl, co = co0 + c;
+                    if (co >= a.Co)
+                        break;
+                    pw_store4<T>(a, p, co, c, acc[f], s_scale, s_bias);
+                }
             }
         }
     }
