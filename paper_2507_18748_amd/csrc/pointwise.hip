@@ -32,7 +32,7 @@
 // tap 4 ks + q, gathering the C channels of the input pixel under that tap
 // for its output pixel (zero outside the image) and reading the tap's weight
 // vector from LDS, where the block stages its channel slice once.  The same
-// epilogue follows; fp32 stems run on the 16x16x4 fp32 MFMA.
+// row-contiguous epilogue follows; fp32 stems run on the 16x16x4 fp32 MFMA.
 #include "kernels.h"
 
 #include <algorithm>
@@ -124,6 +124,71 @@ __device__ __forceinline__ void pw_store4(const ConvGemmArgs& a, int p, int co, 
     }
 }
 
+// Row-contiguous epilogue of one 16-pixel group (output channels a multiple
+// of the 16-byte vector): the wave stages the scaled sums as a [16 pixel]
+// [16 CF channel] fp32 tile in its own LDS rows tw (row pitch TROW floats),
+// then every lane finishes one 16-byte vector of one pixel (residual,
+// activation, rounding) and stores it, so consecutive lanes write along each
+// pixel's channel row instead of 8- or 16-byte pieces of 16 rows.
+template <int CF>
+constexpr int pw_trow() { return CF * 16 + 4; }
+template <typename T, int CF>
+__device__ __forceinline__ void pw_rows_store(const ConvGemmArgs& a, const floatx4 (&acc)[CF],
+                                              const float* __restrict__ s_scale,
+                                              const float* __restrict__ s_bias,
+                                              float* __restrict__ tw, int g, int co0, int lane)
+{
+    constexpr int VE = 16 / (int)sizeof(T);     // channels per 16-byte vector
+    constexpr int NV = 16 * CF / VE;            // vectors of a pixel's slice
+    constexpr int NIT = (16 * NV + 63) / 64;    // vectors per lane and group
+    constexpr int TROW = pw_trow<CF>();
+    const int cl = 4 * (lane >> 4);
+#pragma unroll
+    for (int f = 0; f < CF; ++f) {
+        const int c = 16 * f + cl;
+        const float4 sc = *(const float4*)(s_scale + c);   // 16-byte aligned arrays
+        const float4 bi = *(const float4*)(s_bias + c);
+        float4 v;
+        v.x = acc[f][0] * sc.x + bi.x;
+        v.y = acc[f][1] * sc.y + bi.y;
+        v.z = acc[f][2] * sc.z + bi.z;
+        v.w = acc[f][3] * sc.w + bi.w;
+        *(float4*)(tw + (lane & 15) * TROW + c) = v;
+    }
+    __builtin_amdgcn_wave_barrier();   // one wave's LDS operations run in order
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+        const int v = it * 64 + lane;
+        const int px = v / NV, cv = v - px * NV;
+        const int p = g * 16 + px, co = co0 + VE * cv;
+        if (v < 16 * NV && p < a.M && co < a.Co) {
+            const size_t off = (size_t)p * a.Co + co;
+            uint4 r = make_uint4(0u, 0u, 0u, 0u);
+            if (a.res)
+                r = *(const uint4*)((const T*)a.res + off);
+            float o[VE];
+#pragma unroll
+            for (int q = 0; q < VE; q += 4) {
+                const float4 t = *(const float4*)(tw + px * TROW + VE * cv + q);
+                o[q] = t.x; o[q + 1] = t.y; o[q + 2] = t.z; o[q + 3] = t.w;
+            }
+            if (a.res) {
+                T rr[VE];
+                __builtin_memcpy(rr, &r, 16);
+#pragma unroll
+                for (int q = 0; q < VE; ++q) o[q] += (float)rr[q];
+            }
+            T e[VE];
+#pragma unroll
+            for (int q = 0; q < VE; ++q) e[q] = (T)pw_act(o[q], a.act);
+            uint4 u;
+            __builtin_memcpy(&u, e, 16);
+            *(uint4*)((T*)a.y + off) = u;
+        }
+    }
+    __builtin_amdgcn_wave_barrier();
+}
+
 // Block: PW_WAVES waves on output channels [co0, co0 + 16 CF); blockIdx.y is
 // the channel slice, waves of all blocks along x share the pixel groups.
 // KS: 32-element k-steps (C <= 32 KS); groups in flight ahead of the one
@@ -133,17 +198,10 @@ __global__ void __launch_bounds__(PW_WAVES * 64) pw_conv_kernel(ConvGemmArgs a)
 {
     constexpr int PW_PF = KS == 1 ? 3 : 1;
     constexpr int ESZ = (int)sizeof(T);
-    __shared__ float s_scale[CF * 16], s_bias[CF * 16];
-    // Row-contiguous stores: a wave stages its group's scaled sums as a
-    // [16 pixel][16 CF channel] fp32 tile in its own LDS rows, then every lane
-    // finishes one 8-channel vector of one pixel (residual, activation,
-    // rounding) and stores 16 contiguous bytes, so consecutive lanes write
-    // along each pixel's channel row instead of 32-byte pieces of 16 rows.
-    constexpr int NV = 2 * CF;                  // 8-channel vectors of a pixel's slice
-    constexpr int NIT = (16 * NV + 63) / 64;    // vectors per lane and group
-    constexpr int TROW = CF * 16 + 4;           // floats per staged pixel row
-    __shared__ __attribute__((aligned(16))) float s_tile[PW_WAVES][16][TROW];
-    const bool rows_out = a.Co % 8 == 0;
+    __shared__ __attribute__((aligned(16))) float s_scale[CF * 16], s_bias[CF * 16];
+    // each wave's rows of the row-contiguous epilogue (pw_rows_store)
+    __shared__ __attribute__((aligned(16))) float s_tile[PW_WAVES][16][pw_trow<CF>()];
+    const bool rows_out = a.Co % (16 / ESZ) == 0;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -203,46 +261,7 @@ __global__ void __launch_bounds__(PW_WAVES * 64) pw_conv_kernel(ConvGemmArgs a)
             for (int ks = 0; ks < KS; ++ks) bq[d][ks] = bq[d + 1][ks];
 
         if (rows_out) {
-            float* tw = &s_tile[wave][0][0];
-#pragma unroll
-            for (int f = 0; f < CF; ++f) {
-                const int c = 16 * f + cl;
-                float4 v;
-                v.x = acc[f][0] * s_scale[c] + s_bias[c];
-                v.y = acc[f][1] * s_scale[c + 1] + s_bias[c + 1];
-                v.z = acc[f][2] * s_scale[c + 2] + s_bias[c + 2];
-                v.w = acc[f][3] * s_scale[c + 3] + s_bias[c + 3];
-                *(float4*)(tw + (lane & 15) * TROW + c) = v;
-            }
-            __builtin_amdgcn_wave_barrier();   // one wave's LDS operations run in order
-#pragma unroll
-            for (int it = 0; it < NIT; ++it) {
-                const int v = it * 64 + lane;
-                const int px = v / NV, cv = v - px * NV;
-                const int p = g * 16 + px, co = co0 + 8 * cv;
-                if (v < 16 * NV && p < a.M && co < a.Co) {
-                    const size_t off = (size_t)p * a.Co + co;
-                    uint4 r = make_uint4(0u, 0u, 0u, 0u);
-                    if (a.res)
-                        r = *(const uint4*)((const T*)a.res + off);
-                    const float4 lo = *(const float4*)(tw + px * TROW + 8 * cv);
-                    const float4 hi = *(const float4*)(tw + px * TROW + 8 * cv + 4);
-                    float o[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-                    if (a.res) {
-                        T rr[8];
-                        __builtin_memcpy(rr, &r, 16);
-#pragma unroll
-                        for (int q = 0; q < 8; ++q) o[q] += (float)rr[q];
-                    }
-                    T e[8];
-#pragma unroll
-                    for (int q = 0; q < 8; ++q) e[q] = (T)pw_act(o[q], a.act);
-                    uint4 u;
-                    __builtin_memcpy(&u, e, 16);
-                    *(uint4*)((T*)a.y + off) = u;
-                }
-            }
-            __builtin_amdgcn_wave_barrier();
+            pw_rows_store<T, CF>(a, acc, s_scale, s_bias, &s_tile[wave][0][0], g, co0, lane);
         } else {
             const int p = g * 16 + (lane & 15);
             if (p < a.M) {
@@ -266,9 +285,12 @@ __global__ void __launch_bounds__(PW_WAVES * 64) stem_conv_kernel(ConvGemmArgs a
     constexpr int ESZ = (int)sizeof(T);
     constexpr int EPV = 16 / ESZ;
     constexpr int ROWS = CF * 16;
-    __shared__ float s_scale[ROWS], s_bias[ROWS];
+    __shared__ __attribute__((aligned(16))) float s_scale[ROWS], s_bias[ROWS];
     // weights [ks][row][4 taps x 16 bytes]: a fragment read is 1 KB contiguous
     __shared__ uint4 s_w[KST * ROWS * 4];
+    // each wave's rows of the row-contiguous epilogue (pw_rows_store)
+    __shared__ __attribute__((aligned(16))) float s_tile[PW_WAVES][16][pw_trow<CF>()];
+    const bool rows_out = a.Co % EPV == 0;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int co0 = blockIdx.y * ROWS;
@@ -329,7 +351,9 @@ __global__ void __launch_bounds__(PW_WAVES * 64) stem_conv_kernel(ConvGemmArgs a
             for (int f = 0; f < CF; ++f)
                 acc[f] = pw_mfma<T>(s_w[(ks * ROWS + 16 * f + (lane & 15)) * 4 + q], b, acc[f]);
         }
-        if (p < a.M) {
+        if (rows_out) {
+            pw_rows_store<T, CF>(a, acc, s_scale, s_bias, &s_tile[wave][0][0], g, co0, lane);
+        } else if (p < a.M) {
 #pragma unroll
             for (int f = 0; f < CF; ++f) {
                 const int c = 16 * f + cl, co = co0 + c;
