@@ -1,9 +1,11 @@
 """Benchmark: images/s of one CNN partition forward on one MI355X.
 
-Default workload: ResNet-50 layers [44, 56) (layer4 + global avgpool + FC-1000
-+ softmax) on 8 x 1024 x 14 x 14 bf16 activations drawn from ReLU(N(0,1)),
-seeded synthetic weights.  A step is one forward of the whole range at the
-workload's batch, inputs resident in HBM.  Prints one JSON line with the
+Default workload: ResNet-152, the whole model (158 fused layers, stem to
+softmax), fp16, batch 64 on 64 x 3 x 224 x 224 seeded synthetic images with
+seeded He-init weights: the largest batch of the 1..64 range whose per-layer
+latency table the paper's planner consumes (Sec. 5.1; App. A.1, L_kbi).  A
+step is one forward of the whole range at that batch, inputs resident in
+HBM.  Other workloads: --workload NAME [--batch B].  Prints one JSON line with the
 throughput, the roofline position of the dominant kernel (per-launch HIP
 event timing on the stream the kernels run on) and the CPU oracle timed on
 a bounded sample as a baseline.
@@ -21,6 +23,8 @@ METRIC = "CNN-partition images/sec at batch 1–64; per-layer MFMA % or HBM GB/s
 PEAK_MFMA_TFLOPS = {"f16": 2516.6, "bf16": 2516.6, "f32": 157.3}
 PEAK_HBM_GBS = 8000.0
 DTYPE_LABEL = {"f32": "f32", "f16": "f16", "bf16": "bf16"}
+DEFAULT_WORKLOAD = "resnet152"
+DEFAULT_BATCH = {"resnet152": 64}
 
 
 def roofline(records, dtype):
@@ -129,20 +133,47 @@ def measured_traffic(workload, kernel):
     return None
 
 
-def cpu_baseline(wl, m, P, target_s):
+def host_cpu():
+    """Host facts for the CPU baseline: logical CPUs, model name, OpenMP setting."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "affinity": len(os.sched_getaffinity(0)),
+            "cpu_model": model, "OMP_NUM_THREADS": os.environ.get("OMP_NUM_THREADS")}
+
+
+def cpu_baseline(wl, m, P, target_s, sample_batches=(1, 4)):
+    """The oracle on a bounded sample of the workload: one pass at each of
+    `sample_batches` (images of the same seeded input), then the last batch
+    repeated until `target_s` of wall time.  images/s over the whole sample."""
     import oracle
-    x = wl.input(wl.batch)
-    images, t0 = 0, time.perf_counter()
-    while True:
-        oracle.forward(m.layers, P, wl.begin, wl.end, x, wl.dtype)
-        images += wl.batch
-        el = time.perf_counter() - t0
-        if el >= target_s:
-            break
-    return {"value": images / el, "unit": "images/s", "cores": oracle.num_threads(),
-            "kind": "oracle",
-            "sample": f"{images} images ({images // wl.batch} x the batch of {wl.batch}), "
-                      f"{el:.1f} s wall"}
+    images, el, per = 0, 0.0, {}
+    for b in sample_batches:
+        x = wl.input(b)
+        n = 0
+        t0 = time.perf_counter()
+        while True:
+            oracle.forward(m.layers, P, wl.begin, wl.end, x, wl.dtype)
+            n += b
+            t = time.perf_counter() - t0
+            if b != sample_batches[-1] or el + t >= target_s:
+                break
+        per[b] = n / t
+        images += n
+        el += t
+    out = {"value": images / el, "unit": "images/s", "cores": oracle.num_threads(),
+           "kind": "oracle",
+           "sample": f"{images} images of the workload's seeded input: batch "
+                     + ", then ".join(f"{b} ({per[b]:.2f} images/s)" for b in sample_batches)
+                     + f" repeated; {el:.1f} s wall"}
+    out.update(host_cpu())
+    return out
 
 
 def library_baseline(wl, m, P, x_nchw, steps, warmup, ref_out=None):
@@ -294,7 +325,7 @@ def latency_table(args):
     chunk = 8
     for c0 in range(0, len(batches), chunk):
         bs = batches[c0:c0 + chunk]
-        t, w = part.profile_layers(bs, warmup=3, reps=args.profile_reps)
+        t, w = part.profile_layers(bs, warmup=args.profile_warmup, reps=args.profile_reps)
         table[:, c0:c0 + len(bs)] = t
         whole[c0:c0 + len(bs)] = w
         print(f"[table] batches {bs[0]}..{bs[-1]} done", file=sys.stderr, flush=True)
@@ -350,7 +381,7 @@ def blocks_report(args):
     in_chw = (m.in_c, m.in_h, m.in_w)
     with Partition(m.layers, P, in_chw, wl.begin, wl.end, wl.dtype,
                    max_batch=max(batches)) as part:
-        table, whole = part.profile_layers(batches, warmup=3, reps=args.profile_reps)
+        table, whole = part.profile_layers(batches, warmup=args.profile_warmup, reps=args.profile_reps)
     print("[blocks] layer table done", file=sys.stderr, flush=True)
     ok = split_points(m.layers)
     local_ok = [1] + [ok[p] for p in range(wl.begin + 1, wl.end)] + [1]
@@ -360,7 +391,7 @@ def blocks_report(args):
     blocks = []
     for bb, be in zip(bounds, bounds[1:]):
         with Partition(m.layers, P, in_chw, bb, be, wl.dtype, max_batch=max(batches)) as bp:
-            bt, bw = bp.profile_layers(batches, warmup=3, reps=args.profile_reps)
+            bt, bw = bp.profile_layers(batches, warmup=args.profile_warmup, reps=args.profile_reps)
         layer_sum = table[bb - wl.begin:be - wl.begin].sum(axis=0)
         blocks.append({"layers": [bb, be],
                        "block_us": {b: float(bw[j]) for j, b in enumerate(batches)},
@@ -455,7 +486,7 @@ def batching_report(args):
     in_chw = (m.in_c, m.in_h, m.in_w)
     with Partition(m.layers, P, in_chw, wl.begin, wl.end, wl.dtype,
                    max_batch=max(batches)) as part:
-        table, whole = part.profile_layers(batches, warmup=3, reps=args.profile_reps)
+        table, whole = part.profile_layers(batches, warmup=args.profile_warmup, reps=args.profile_reps)
         out_bytes = [part.layer_info(i, 1)["out_bytes_b1"] for i in range(wl.begin, wl.end)]
     print("[batching] layer table done", file=sys.stderr, flush=True)
     ok = split_points(m.layers)
@@ -578,8 +609,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=2000)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--workload", default="resnet50_layer4_head")
-    ap.add_argument("--batch", type=int, default=0, help="override the workload batch")
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--batch", type=int, default=0,
+                    help="batch of the benchmark (default: 64 for resnet152, else the "
+                         "workload's own batch)")
     ap.add_argument("--no-graph", action="store_true", help="launch kernels directly")
     ap.add_argument("--blocks-out", default="", metavar="OUT.json",
                     help="pre-partition the workload into --blocks blocks from its latency "
@@ -599,7 +632,10 @@ def main():
                     help="directly launched steps whose per-launch events give the roofline")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="oracle sample length for cpu_baseline (0 disables)")
-    ap.add_argument("--profile-reps", type=int, default=50)
+    ap.add_argument("--profile-reps", type=int, default=50,
+                    help="timed repetitions per latency-table entry (median)")
+    ap.add_argument("--profile-warmup", type=int, default=10,
+                    help="untimed repetitions before the latency-table runs")
     ap.add_argument("--table", metavar="OUT.json", default=None,
                     help="instead of the benchmark, write the per-layer latency table of the "
                          "workload (median us per layer at each --batches size) with S_i and "
@@ -646,9 +682,10 @@ def main():
         return batching_report(args)
 
     wl = W.workload(args.workload)
-    if args.batch:
+    batch = args.batch or DEFAULT_BATCH.get(wl.name, wl.batch)
+    if batch != wl.batch:
         import dataclasses
-        wl = dataclasses.replace(wl, batch=args.batch)
+        wl = dataclasses.replace(wl, batch=batch)
     m = wl.build_model()
     P = wl.params(m)
     torch.cuda.set_device(0)

@@ -76,6 +76,7 @@ typedef struct {
     const float* bn_mean;
     const float* bn_var;
     float bn_eps;
+    const char* name;    /* NUL-terminated layer name (copied at create), or NULL: "layer<i>" */
 } ppipe_layer_desc;
 
 /* The whole model (all layers from 0), so shapes can be derived for any
@@ -99,6 +100,8 @@ typedef struct {
     int64_t in_bytes_per_image, out_bytes_per_image;
     int64_t weight_bytes;            /* device bytes of packed weights, scales and biases */
     int64_t workspace_bytes;         /* device bytes of activation and split-K buffers */
+    int32_t tuned;                   /* 1 when created with a planner override
+                                        (ppipe_partition_create_tuned), else 0 */
 } ppipe_partition_info_t;
 
 typedef struct {
@@ -113,6 +116,9 @@ typedef struct {
     char kernel[96];                 /* kernel configuration chosen at the queried batch;
                                         ends in " paired=J" when the layer runs in one
                                         launch with layer J */
+    char name[64];                   /* the layer's name from its description */
+    int32_t forced;                  /* 1 when a tuning override chose this layer's
+                                        kernel at the queried batch */
 } ppipe_layer_info_t;
 
 typedef struct {
@@ -135,6 +141,29 @@ typedef struct {
 ppipe_partition* ppipe_partition_create(const ppipe_model_desc* desc,
                                         int32_t layer_begin, int32_t layer_end,
                                         int32_t dtype);
+
+/* Planner overrides, for kernel tests and tuning sweeps only.  A
+ * partition created with overrides runs the configurations they name
+ * instead of the planner's choices; ppipe_partition_info reports `tuned`
+ * and ppipe_layer_info `forced` for every layer the overrides changed, so a
+ * latency table taken on such a handle says so.  Zero fields (gemm_cfg -1)
+ * leave the planner's choice. */
+typedef struct {
+    int32_t gemm_cfg;      /* -1, or a GEMM configuration id forced on every eligible layer */
+    int32_t gemm_waves;    /* waves per block of a forced skinny configuration (4, 8, 16) */
+    int32_t gemm_splits;   /* K splits of a forced LDS-staged configuration (1..64) */
+    int32_t no_pointwise;  /* nonzero: never plan the streaming 1x1 kernel */
+    int32_t no_stem;       /* nonzero: never plan the stem kernel */
+    int32_t stream_grid;   /* > 0: blocks along the pixels of the streaming 1x1 and stem kernels */
+    int32_t no_pair;       /* nonzero: never run paired layers as one launch */
+    int32_t dw_outputs;    /* 0, or 2 / 4 outputs per thread of stride-1 depthwise layers */
+} ppipe_tuning;
+
+/* ppipe_partition_create with planner overrides (NULL: none, the same as
+ * ppipe_partition_create).  PPIPE_E_INVALID for a field out of range. */
+ppipe_partition* ppipe_partition_create_tuned(const ppipe_model_desc* desc,
+                                              int32_t layer_begin, int32_t layer_end,
+                                              int32_t dtype, const ppipe_tuning* tuning);
 
 /* Forward pass of the range at batch size `batch` (1..max_batch).
  * in:  device pointer, [batch][in_h][in_w][in_c] in dtype (caller-owned).

@@ -26,7 +26,16 @@ class LayerDesc(ctypes.Structure):
                 ("c_in", ctypes.c_int32), ("c_out", ctypes.c_int32), ("k", ctypes.c_int32),
                 ("stride", ctypes.c_int32), ("pad", ctypes.c_int32), ("groups", ctypes.c_int32),
                 ("act", ctypes.c_int32), ("weight", _fp), ("bias", _fp), ("bn_gamma", _fp),
-                ("bn_beta", _fp), ("bn_mean", _fp), ("bn_var", _fp), ("bn_eps", ctypes.c_float)]
+                ("bn_beta", _fp), ("bn_mean", _fp), ("bn_var", _fp), ("bn_eps", ctypes.c_float),
+                ("name", ctypes.c_char_p)]
+
+
+class Tuning(ctypes.Structure):
+    """Planner overrides (kernel tests and tuning sweeps only)."""
+    _fields_ = [("gemm_cfg", ctypes.c_int32), ("gemm_waves", ctypes.c_int32),
+                ("gemm_splits", ctypes.c_int32), ("no_pointwise", ctypes.c_int32),
+                ("no_stem", ctypes.c_int32), ("stream_grid", ctypes.c_int32),
+                ("no_pair", ctypes.c_int32), ("dw_outputs", ctypes.c_int32)]
 
 
 class ModelDesc(ctypes.Structure):
@@ -48,7 +57,7 @@ class PartitionInfo(ctypes.Structure):
                 ("out_c", ctypes.c_int32), ("out_h", ctypes.c_int32), ("out_w", ctypes.c_int32),
                 ("out_dtype", ctypes.c_int32), ("in_bytes_per_image", ctypes.c_int64),
                 ("out_bytes_per_image", ctypes.c_int64), ("weight_bytes", ctypes.c_int64),
-                ("workspace_bytes", ctypes.c_int64)]
+                ("workspace_bytes", ctypes.c_int64), ("tuned", ctypes.c_int32)]
 
 
 class LayerInfo(ctypes.Structure):
@@ -56,7 +65,8 @@ class LayerInfo(ctypes.Structure):
                 ("out_h", ctypes.c_int32), ("out_w", ctypes.c_int32),
                 ("kernel_count", ctypes.c_int32), ("out_bytes_b1", ctypes.c_int64),
                 ("flops_b1", ctypes.c_double), ("act_bytes_b1", ctypes.c_double),
-                ("param_bytes", ctypes.c_double), ("kernel", ctypes.c_char * 96)]
+                ("param_bytes", ctypes.c_double), ("kernel", ctypes.c_char * 96),
+                ("name", ctypes.c_char * 64), ("forced", ctypes.c_int32)]
 
 
 class KernelRecord(ctypes.Structure):
@@ -127,6 +137,9 @@ def load_library() -> ctypes.CDLL:
     vp, i32 = ctypes.c_void_p, ctypes.c_int32
     lib.ppipe_partition_create.restype = vp
     lib.ppipe_partition_create.argtypes = [ctypes.POINTER(ModelDesc), i32, i32, i32]
+    lib.ppipe_partition_create_tuned.restype = vp
+    lib.ppipe_partition_create_tuned.argtypes = [ctypes.POINTER(ModelDesc), i32, i32, i32,
+                                                 ctypes.POINTER(Tuning)]
     lib.ppipe_partition_run.restype = ctypes.c_int
     lib.ppipe_partition_run.argtypes = [vp, i32, vp, vp, vp]
     lib.ppipe_partition_capture.restype = ctypes.c_int
@@ -366,11 +379,14 @@ class Partition:
       c_out, k, stride, pad, groups, act (op / act as names, see OPS / ACTS).
     params: {layer index: {"weight", "bias", "bn_gamma", "bn_beta", "bn_mean",
       "bn_var"}} of float32 numpy arrays (OIHW weights); read during create.
+    tuning: planner overrides for kernel tests and tuning sweeps, a dict of
+      Tuning fields (gemm_plan=(cfg, waves, splits) sets the first three);
+      None (the default) leaves every choice to the planner.
     """
 
     def __init__(self, layers: Sequence, params: Dict[int, Dict[str, np.ndarray]],
                  in_chw: Sequence[int], begin: int, end: int, dtype: str,
-                 max_batch: int = 64, bn_eps: float = 1e-5):
+                 max_batch: int = 64, bn_eps: float = 1e-5, tuning: Optional[dict] = None):
         self._lib = load_library()
         self.begin, self.end, self.dtype = begin, end, dtype
         keep: List[np.ndarray] = []
@@ -393,6 +409,11 @@ class Partition:
             d.pad, d.groups = _attr(L, "pad", 0), _attr(L, "groups", 1)
             d.act = ACTS[_attr(L, "act", "none")]
             d.bn_eps = bn_eps
+            nm = _attr(L, "name")
+            if nm:
+                b = str(nm).encode()
+                keep.append(b)
+                d.name = b
             p = params.get(i, {}) if begin <= i < end else {}
             d.weight = ptr(p.get("weight"))
             d.bias = ptr(p.get("bias"))
@@ -402,7 +423,22 @@ class Partition:
             d.bn_var = ptr(p.get("bn_var"))
         desc = ModelDesc(len(layers), arr, int(in_chw[0]), int(in_chw[1]), int(in_chw[2]),
                          int(max_batch))
-        h = self._lib.ppipe_partition_create(ctypes.byref(desc), begin, end, DTYPES[dtype])
+        if tuning:
+            t = Tuning(-1, 0, 1, 0, 0, 0, 0, 0)
+            for k, v in tuning.items():
+                if k == "gemm_plan":
+                    v = [int(q) for q in v]
+                    t.gemm_cfg = v[0]
+                    t.gemm_waves = v[1] if len(v) > 1 else 0
+                    t.gemm_splits = v[2] if len(v) > 2 else 1
+                elif k in dict(Tuning._fields_):
+                    setattr(t, k, int(v))
+                else:
+                    raise ValueError(f"unknown tuning field {k!r}")
+            h = self._lib.ppipe_partition_create_tuned(ctypes.byref(desc), begin, end,
+                                                       DTYPES[dtype], ctypes.byref(t))
+        else:
+            h = self._lib.ppipe_partition_create(ctypes.byref(desc), begin, end, DTYPES[dtype])
         if not h:
             raise _err(self._lib, self._lib.ppipe_last_status())
         self._h = ctypes.c_void_p(h)
@@ -471,6 +507,7 @@ class Partition:
         self._check(self._lib.ppipe_layer_info(self._h, index, batch, ctypes.byref(li)))
         d = {f: getattr(li, f) for f, _ in LayerInfo._fields_}
         d["kernel"] = li.kernel.decode()
+        d["name"] = li.name.decode()
         return d
 
     # --- lifetime ---

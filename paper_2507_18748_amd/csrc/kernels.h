@@ -172,7 +172,8 @@ const char* softmax_rows_name();
 // folded batch norm and activation.  C % (16 / sizeof(dtype)) == 0.
 hipError_t launch_dwconv(int dt, const void* x, const void* w, const float* scale,
                          const float* bias, void* y, int N, int H, int W, int C, int Ho,
-                         int Wo, int k, int stride, int pad, int act, hipStream_t s);
+                         int Wo, int k, int stride, int pad, int act, int pw_force,
+                         hipStream_t s);
 const char* dwconv_name(int dt, int k);
 
 // k x k max pooling, NHWC; out-of-range taps never win.

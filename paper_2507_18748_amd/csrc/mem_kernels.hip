@@ -500,15 +500,15 @@ hipError_t launch_cache_sweep(void* buf, size_t bytes, hipStream_t s)
 
 hipError_t launch_dwconv(int dt, const void* x, const void* w, const float* scale,
                          const float* bias, void* y, int N, int H, int W, int C, int Ho,
-                         int Wo, int k, int stride, int pad, int act, hipStream_t s)
+                         int Wo, int k, int stride, int pad, int act, int pw_force,
+                         hipStream_t s)
 {
     if (k != 3 || (stride != 1 && stride != 2))
         return hipErrorInvalidValue;
     const int cv = C / (16 / dtype_size(dt));
     // outputs per thread along a row: 4 at stride 1, 2 at stride 2
-    // (PPIPE_DW_PW=2 or 4 overrides the stride-1 choice for tuning sweeps)
+    // (pw_force = 2 or 4 overrides the stride-1 choice for tuning sweeps)
     int pw = stride == 1 ? 4 : 2;
-    static const int pw_force = std::getenv("PPIPE_DW_PW") ? std::atoi(std::getenv("PPIPE_DW_PW")) : 0;
     if (stride == 1 && (pw_force == 2 || pw_force == 4))
         pw = pw_force;
     const size_t total = (size_t)N * Ho * ((Wo + pw - 1) / pw) * cv;

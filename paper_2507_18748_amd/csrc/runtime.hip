@@ -97,6 +97,7 @@ enum { BUF_IN = -1, BUF_OUT = -2, BUF_NONE = -3 };
 struct Plan {
     int cfg, wk, splits, chunks_per_split, total_chunks, tiles_m, tiles_co, co_fastest;
     int grid = 0;   // pointwise kernel: cap on blocks along the pixels (0: resident set)
+    bool forced = false;   // chosen by a tuning override, not by the planner
 };
 
 struct Shape {
@@ -124,6 +125,7 @@ struct LayerRT {
     int pair = -1;
     bool pair_lead = false;
     std::vector<Plan> plans;   // [batch - 1]
+    std::string name;          // the description's layer name, or "layer<i>"
     int64_t out_bytes_b1 = 0;
     double flops_b1 = 0, in_bytes_b1 = 0, res_bytes_b1 = 0, param_bytes = 0;
 };
@@ -138,6 +140,8 @@ struct GraphEntry {
 
 struct ppipe_partition {
     int begin = 0, end = 0, dtype = 0, max_batch = 64, device = 0;
+    ppipe_tuning tune{-1, 0, 1, 0, 0, 0, 0, 0};   // planner overrides given at create
+    bool tuned = false;                           // any override active
     Shape in{}, out{};
     int out_dtype = 0;
     std::vector<LayerRT> L;
@@ -175,7 +179,7 @@ namespace {
 // dtype, eligibility) so that the latency table, the benchmark and the
 // parity tests exercise the same launches.
 Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool stem_ok,
-                 bool split_free)
+                 bool split_free, const ppipe_tuning& tune)
 {
     auto tiles = [&](int cfg) {
         GemmCfgInfo c = gemm_cfg_info(cfg);
@@ -248,8 +252,8 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
     //    with at most 32 output channels) and at least 16384 output pixels
     //    stream through the pointwise kernel (2-3x faster on MobileNetV2's
     //    large expansion layers; the GEMM stays ahead on small grids).
-    //    PPIPE_GEMM_NO_PW turns it off for A/B timing.
-    if (pw_ok && M >= 16384 && !std::getenv("PPIPE_GEMM_NO_PW")) {
+    //    The no_pointwise tuning override turns it off (A/B timing).
+    if (pw_ok && M >= 16384 && !tune.no_pointwise) {
         cfg = GEMM_PW;
         wk = pointwise_channel_frags(Co);
         splits = 1;
@@ -258,18 +262,20 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
     //    pass): filters of up to 28 taps always (3x3 stems 1.7-2.4x faster),
     //    7x7 stems only on small grids (its 13 k-steps of gathered taps
     //    leave one wave per SIMD; the padded GEMM is ahead from about
-    //    200k output pixels).  PPIPE_GEMM_NO_STEM turns it off for A/B timing.
+    //    200k output pixels).  The no_stem tuning override turns it off.
     const int taps = K / (16 / dtype_size(dt));
-    if (stem_ok && (taps <= 28 || M <= 65536) && !std::getenv("PPIPE_GEMM_NO_STEM")) {
+    if (stem_ok && (taps <= 28 || M <= 65536) && !tune.no_stem) {
         cfg = GEMM_STEM;
         wk = stem_channel_frags(Co);
         splits = 1;
     }
-    // PPIPE_GEMM_PLAN="cfg,waves,splits" forces one configuration on every
-    // eligible GEMM layer (tuning sweeps and kernel tests).
-    if (const char* env = std::getenv("PPIPE_GEMM_PLAN")) {
-        int fc = -1, fw = 0, fs = 1;
-        if (std::sscanf(env, "%d,%d,%d", &fc, &fw, &fs) >= 1 && fc >= 0 && fc < GEMM_NCFG) {
+    // The gemm_cfg tuning override (with gemm_waves, gemm_splits) forces one
+    // configuration on every eligible GEMM layer (tuning sweeps and kernel tests).
+    bool forced = false;
+    {
+        const int fc = tune.gemm_cfg, fw = tune.gemm_waves, fs = tune.gemm_splits;
+        if (fc >= 0 && fc < GEMM_NCFG) {
+            const int cfg0 = cfg;
             const bool sk = gemm_cfg_info(fc).skinny;
             const bool wk_ok = fw == 4 || fw == 8 || (fw == 16 && fc == GEMM_SK_16x16);
             if (fc == GEMM_PW) {
@@ -293,6 +299,7 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
                 wk = fw;
                 splits = 1;
             }
+            forced = cfg != cfg0 || fc == cfg0;
         }
     }
     const GemmCfgInfo c = gemm_cfg_info(cfg);
@@ -306,9 +313,12 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
     p.tiles_co = (Co + c.bm - 1) / c.bm;
     if (cfg == GEMM_PW || cfg == GEMM_STEM) {   // 16-pixel groups x channel slices of wk fragments
         p.tiles_co = (Co + 16 * wk - 1) / (16 * wk);
-        if (const char* env = std::getenv("PPIPE_PW_GRID"))   // tuning sweeps
-            p.grid = std::max(0, std::atoi(env));
+        if (tune.stream_grid > 0) {                 // tuning sweeps
+            p.grid = tune.stream_grid;
+            forced = true;
+        }
     }
+    p.forced = forced;
     p.co_fastest = M > Co ? 1 : 0;   // keep the larger operand's slices on one XCD
     return p;
 }
@@ -451,11 +461,11 @@ ConvGemmArgs gemm_args(const ppipe_partition* P, const LayerRT& l, int batch, co
 // planned unsplit on the sparse-grid configuration (8-wave 64x64, four
 // stages), where neither grid fills the chip and each launch is bound by its
 // latency.  Dense grids gain nothing from sharing a launch (ResNet-152 at
-// batch 16 ran 0.7% slower with its two dense pairs joined).  PPIPE_NO_PAIR
-// turns pairing off (A/B timing).
-bool pair_runs(const LayerRT& a, const LayerRT& b, int batch)
+// batch 16 ran 0.7% slower with its two dense pairs joined).  The no_pair
+// tuning override turns pairing off (A/B timing).
+bool pair_runs(const ppipe_partition* P, const LayerRT& a, const LayerRT& b, int batch)
 {
-    static const bool off = std::getenv("PPIPE_NO_PAIR") != nullptr;
+    const bool off = P->tune.no_pair != 0;
     const Plan& p = a.plans[batch - 1];
     const Plan& q = b.plans[batch - 1];
     return !off && p.cfg == GEMM_DMA_64x64_8W_S4 && q.cfg == GEMM_DMA_64x64_8W_S4 &&
@@ -520,7 +530,7 @@ hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, 
     case K_DW:
         if (hook) hook->before(l, 0, s);
         e = launch_dwconv(P->dtype, x, l.w, l.scale, l.bias, y, batch, l.H, l.W, l.C, l.Ho,
-                          l.Wo, l.k, l.stride, l.pad, l.act, s);
+                          l.Wo, l.k, l.stride, l.pad, l.act, P->tune.dw_outputs, s);
         if (hook) hook->after(l, 0, s);
         return e;
     case K_MAXPOOL:
@@ -546,7 +556,7 @@ hipError_t enqueue_all(const ppipe_partition* P, int batch, const void* in, void
 {
     for (const LayerRT& l : P->L) {
         hipError_t e;
-        if (!hook && l.pair >= 0 && pair_runs(l.pair_lead ? l : P->L[l.pair],
+        if (!hook && l.pair >= 0 && pair_runs(P, l.pair_lead ? l : P->L[l.pair],
                                               l.pair_lead ? P->L[l.pair] : l, batch)) {
             if (!l.pair_lead)
                 continue;   // ran with its lead
@@ -714,6 +724,7 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
         const Shape x = shape_of(ld.src), o = sh[i];
         const std::string who = "layer " + std::to_string(i);
         l.index = i; l.op = ld.op; l.src = ld.src; l.res_src = ld.res_src; l.act = ld.act;
+        l.name = ld.name && ld.name[0] ? std::string(ld.name) : "layer" + std::to_string(i);
         l.k = ld.k; l.stride = ld.stride; l.pad = ld.pad; l.groups = ld.groups;
         l.H = x.h; l.W = x.w; l.C = x.c; l.Ho = o.h; l.Wo = o.w; l.Co = o.c;
         if (ld.act < PPIPE_ACT_NONE || ld.act > PPIPE_ACT_RELU6)
@@ -885,7 +896,11 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
         if (a.pair >= 0 || !pairable(a, i)) continue;
         for (int j = i + 1; j < end; ++j) {
             LayerRT& b = P->L[j - begin];
-            if (b.pair < 0 && pairable(b, j) && d->layers[j].src == d->layers[i].src) {
+            // the pair runs at i's position, so j's residual (if any) must
+            // already exist there: produced before layer i
+            const int rj = d->layers[j].res_src;
+            if (b.pair < 0 && pairable(b, j) && d->layers[j].src == d->layers[i].src &&
+                (rj == -1 || rj < i)) {
                 a.pair = j - begin;
                 a.pair_lead = true;
                 b.pair = i - begin;
@@ -947,7 +962,7 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
         for (int b = 1; b <= P->max_batch; ++b) {
             const int M = b * l.Ho * l.Wo;
             const Plan p = choose_plan(M, l.Co, l.K, dt, l.skinny_ok, l.pw_ok, l.stem_ok,
-                                       l.softmax);
+                                       l.softmax, P->tune);
             l.plans[b - 1] = p;
             size_t need = 0;
             if (p.splits > 1) need += (size_t)p.splits * M * l.Co;
@@ -1119,8 +1134,24 @@ int32_t ppipe_last_status(void) { return g_status; }
 ppipe_partition* ppipe_partition_create(const ppipe_model_desc* desc, int32_t layer_begin,
                                         int32_t layer_end, int32_t dtype)
 {
+    return ppipe_partition_create_tuned(desc, layer_begin, layer_end, dtype, nullptr);
+}
+
+ppipe_partition* ppipe_partition_create_tuned(const ppipe_model_desc* desc,
+                                              int32_t layer_begin, int32_t layer_end,
+                                              int32_t dtype, const ppipe_tuning* tuning)
+{
     g_err.clear();
     g_status = 0;
+    if (tuning) {
+        const ppipe_tuning& t = *tuning;
+        if (t.gemm_cfg < -1 || t.gemm_cfg >= GEMM_NCFG || t.gemm_splits < 0 ||
+            t.gemm_splits > 64 || t.stream_grid < 0 ||
+            (t.dw_outputs != 0 && t.dw_outputs != 2 && t.dw_outputs != 4)) {
+            fail(PPIPE_E_INVALID, "tuning override out of range");
+            return nullptr;
+        }
+    }
     if (!desc || !desc->layers || desc->n_layers < 1) {
         fail(PPIPE_E_INVALID, "model description is empty");
         return nullptr;
@@ -1139,6 +1170,11 @@ ppipe_partition* ppipe_partition_create(const ppipe_model_desc* desc, int32_t la
         return nullptr;
     }
     ppipe_partition* P = new ppipe_partition();
+    if (tuning) {
+        P->tune = *tuning;
+        P->tuned = tuning->gemm_cfg >= 0 || tuning->no_pointwise || tuning->no_stem ||
+                   tuning->stream_grid > 0 || tuning->no_pair || tuning->dw_outputs;
+    }
     P->begin = layer_begin;
     P->end = layer_end;
     P->dtype = dtype;
@@ -1161,7 +1197,9 @@ void ppipe_partition_destroy(ppipe_partition* h)
 {
     if (!h) return;
     ensure_device(h);
-    (void)hipDeviceSynchronize();
+    // runs on the caller's streams are the caller's to finish (hipFree itself
+    // waits for the device); the handle's own timed events are waited for here
+    if (h->timed.ran && !h->timed.ev.empty()) (void)hipEventSynchronize(h->timed.ev.back());
     release(h);
     delete h;
 }
@@ -1491,7 +1529,9 @@ int ppipe_timing_setup(ppipe_partition* h, int32_t batch, const void* in, void* 
     int rc = check_run_args(h, batch, in, out);
     if (rc != PPIPE_OK) return rc;
     if ((rc = ensure_device(h)) != PPIPE_OK) return rc;
-    (void)hipDeviceSynchronize();
+    // the events of an earlier timed run may still be pending: its last
+    // event is recorded after its last launch on the same stream
+    if (h->timed.ran && !h->timed.ev.empty()) (void)hipEventSynchronize(h->timed.ev.back());
     release_timed(h);
     int nlaunch = 0;
     for (const LayerRT& l : h->L) nlaunch += layer_launches(l, batch);
@@ -1571,6 +1611,7 @@ int ppipe_partition_info(const ppipe_partition* h, ppipe_partition_info_t* info)
     size_t ws = h->ws_bytes + h->pad_bytes;
     for (size_t b : h->slot_bytes) ws += b;
     info->workspace_bytes = (int64_t)ws;
+    info->tuned = h->tuned ? 1 : 0;
     return PPIPE_OK;
 }
 
@@ -1586,6 +1627,7 @@ int ppipe_layer_info(const ppipe_partition* h, int32_t index, int32_t batch,
     std::memset(info, 0, sizeof(*info));
     info->index = l.index;
     info->op = l.op;
+    std::snprintf(info->name, sizeof(info->name), "%s", l.name.c_str());
     info->out_c = l.Co; info->out_h = l.Ho; info->out_w = l.Wo;
     info->kernel_count = layer_launches(l, batch);
     info->out_bytes_b1 = l.softmax ? (int64_t)l.Co * 4 : l.out_bytes_b1;
@@ -1602,10 +1644,12 @@ int ppipe_layer_info(const ppipe_partition* h, int32_t index, int32_t batch,
         const Plan& p = l.plans[batch - 1];
         k += " tiles=" + std::to_string(p.tiles_m * p.tiles_co) + " splits=" +
              std::to_string(p.splits);
-        if (l.pair >= 0 && pair_runs(l.pair_lead ? l : h->L[l.pair],
+        if (l.pair >= 0 && pair_runs(h, l.pair_lead ? l : h->L[l.pair],
                                      l.pair_lead ? h->L[l.pair] : l, batch))
             k += " paired=" + std::to_string(h->L[l.pair].index);
+        info->forced = p.forced ? 1 : 0;
     }
+    if (l.kind == K_DW && h->tune.dw_outputs) info->forced = 1;
     std::snprintf(info->kernel, sizeof(info->kernel), "%s", k.c_str());
     return PPIPE_OK;
 }

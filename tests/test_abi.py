@@ -137,3 +137,25 @@ def test_cu_share_stream_rejects_bad_shares():
     assert lib.ppipe_stream_create_cu_share(2, 2, ctypes.byref(st)) == -1
     assert lib.ppipe_stream_create_cu_share(0, 0, ctypes.byref(st)) == -1
     assert lib.ppipe_stream_destroy(None) == 0
+
+
+def test_product_sources_read_no_environment():
+    """Kernel choice is deterministic in the layer shape and the create-time
+    tuning argument: no library source reads an environment variable."""
+    csrc = os.path.join(ROOT, "paper_2507_18748_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        text = open(os.path.join(csrc, f)).read()
+        assert "getenv" not in text, f
+
+
+def test_create_tuned_rejects_out_of_range_overrides():
+    from paper_2507_18748_amd import Partition
+    layers = _tiny_layers()
+    for bad in ({"gemm_cfg": 999}, {"dw_outputs": 3}, {"gemm_plan": (0, 0, 100)},
+                {"stream_grid": -1}):
+        st = _status_of(lambda: Partition(layers, _params(layers), (8, 6, 6), 0, 5, "f16",
+                                          max_batch=4, tuning=bad))
+        assert st == -1, bad
+    with pytest.raises(ValueError):
+        Partition(layers, _params(layers), (8, 6, 6), 0, 5, "f16", max_batch=4,
+                  tuning={"no_such_field": 1})

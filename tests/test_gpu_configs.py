@@ -1,22 +1,24 @@
 """Parity of the five workloads at their full shapes and batch sizes,
 through the C ABI, against the CPU oracle on the same seeded inputs.
 
-Two checks per workload:
+Checks per workload:
  * segment parity: the range is cut at every point where exactly one feature
    map crosses (every valid partition boundary); each minimal segment is run
    on the GPU from the oracle's own stored input and compared element by
-   element with the oracle's output of that segment.  This pins every kernel
-   launch at its real shape and batch to the stated tolerance.
+   element with the oracle's output of that segment, within a few storage
+   roundings (SEG_TOL).  This pins every kernel launch at its real shape and
+   batch.
  * end to end: the whole range on the GPU vs the oracle.  Tolerance: infinity-
    norm relative error <= 2e-2 for fp16/bf16 storage, 1e-4 for fp32, argmax of
-   the class probabilities bit-exact.  Two bf16 ranges (MobileNetV2 and
-   ResNet-50 layer3+layer4) are ill-conditioned under random initialisation:
-   a one-ulp storage difference at an early layer grows through the network,
-   so no implementation whose sums differ from the oracle's fp64 sums meets
-   2e-2 end to end.  For those the end-to-end error is reported, bounded
-   loosely, and the argmax is required to agree wherever the oracle's
-   top-1/top-2 gap exceeds twice the measured error (where agreement is
-   implied by the error bound); their element-wise bar is the segment check.
+   the class probabilities bit-exact.
+ * two bf16 ranges amplify one-ulp storage differences through depth
+   (tests/test_conditioning.py): on MobileNetV2 at batch 32 every fp32
+   summation order of a correct implementation misses 2e-2 (7.2e-2 .. 9.0e-2,
+   2-4 argmax flips), and on ResNet-50 [25, 56) at batch 8 correct orders
+   land anywhere from 5.3e-3 to 5.1e-2 (a quarter of them above 2e-2).  Their
+   2e-2 tests are expected failures with that reason; in addition the GPU
+   must land inside the envelope of those correct orders (error no larger
+   than the worst order's, no more argmax flips than the worst order's).
 Where the oracle cannot afford the whole batch it checks sampled images of
 the batch the GPU ran (each image's output is independent of the others)."""
 import functools
@@ -32,7 +34,8 @@ from gpu_util import gpu_forward, rel_inf, argmax_rows
 pytestmark = pytest.mark.gpu
 
 TOL = {"f32": 1e-4, "f16": 2e-2, "bf16": 2e-2}
-ILL_CONDITIONED_BOUND = 0.25
+# a segment is one to four fused layers, each rounding its output once
+SEG_TOL = {"f32": 1e-5, "f16": 2.0 ** -9, "bf16": 2.0 ** -7}
 
 
 @functools.lru_cache(maxsize=None)
@@ -94,11 +97,21 @@ def _check_end_to_end(name, batch, sample=None):
     assert agree.all()
 
 
-def _check_ill_conditioned(name, batch):
-    e, agree, gap, pmax = _end_to_end(name, batch)
-    assert e <= ILL_CONDITIONED_BOUND
-    implied = gap > 2 * e * pmax
-    assert agree[implied].all(), "argmax differs where the error bound fixes it"
+def _check_within_fp32_orders(name, orders):
+    """The GPU's end-to-end error against the envelope of correct
+    fp32-accumulating implementations that differ only in summation order."""
+    import conditioning as C
+    wl, m, P = _setup(name)
+    e, agree, _, _ = _end_to_end(name, wl.batch)
+    x = wl.input(wl.batch)
+    _, outs = oracle.forward(m.layers, P, wl.begin, wl.end, x, wl.dtype, keep=True)
+    res = C.ensemble(m.layers, P, wl.begin, wl.end, x, wl.dtype, outs, orders)
+    errs = [r.rel_inf for r in res]
+    flips = [int((~r.argmax_agree).sum()) for r in res]
+    print(f"    {len(res)} fp32 orders: rel_inf {min(errs):.3e} .. {max(errs):.3e}, argmax flips "
+          f"{min(flips)} .. {max(flips)}; GPU {e:.3e}, {int((~agree).sum())} flips", flush=True)
+    assert e <= max(errs)
+    assert int((~agree).sum()) <= max(flips)
 
 
 def _check_segments(name, batch, sample=None):
@@ -123,7 +136,7 @@ def _check_segments(name, batch, sample=None):
         worst = max(worst, e)
         print(f"    segment [{a},{b}) {m.layers[a].name}..{m.layers[b - 1].name}: rel_inf {e:.2e}",
               flush=True)
-        assert e <= TOL[wl.dtype], f"segment [{a},{b}) rel_inf {e:.3e}"
+        assert e <= SEG_TOL[wl.dtype], f"segment [{a},{b}) rel_inf {e:.3e}"
         if m.layers[b - 1].op == "fc_softmax":
             assert (argmax_rows(got) == argmax_rows(ref)).all()
     print(f"[segment-parity] {name} batch {x.shape[0]}: {len(cuts) - 1} segments, "
@@ -140,16 +153,34 @@ def test_resnet50_layer4_head_bf16_batch8():
     _check_end_to_end("resnet50_layer4_head", 8)
 
 
+@pytest.mark.xfail(strict=False, reason=(
+    "whether a correct fp32-accumulating implementation meets 2e-2 on ResNet-50 [25,56) at "
+    "batch 8 (seed 2) depends on its summation order only: 31 orders land at 5.3e-3 .. 5.1e-2, "
+    "26% above 2e-2 (tests/test_conditioning.py); the GPU measured 3.2e-2, 8/8 argmax"))
 def test_resnet50_layer3_layer4_head_bf16_batch8():
-    _check_ill_conditioned("resnet50_layer3_layer4_head", 8)
+    _check_end_to_end("resnet50_layer3_layer4_head", 8)
+
+
+def test_resnet50_layer3_layer4_head_within_fp32_orders():
+    import conditioning as C
+    _check_within_fp32_orders("resnet50_layer3_layer4_head", C.ENSEMBLE_WIDE)
 
 
 def test_vgg16_fp16_batch16():
     _check_end_to_end("vgg16", 16, sample=(0, 7, 15))
 
 
+@pytest.mark.xfail(strict=True, reason=(
+    "no fp32-accumulating implementation meets 2e-2 on MobileNetV2 at batch 32 (seed 4): every "
+    "summation order lands at 7.2e-2 .. 9.0e-2 with 2-4 argmax flips in 32 "
+    "(tests/test_conditioning.py); the GPU measured 6.4e-2 .. 7.0e-2 with 2-3 flips"))
 def test_mobilenet_v2_bf16_batch32():
-    _check_ill_conditioned("mobilenet_v2", 32)
+    _check_end_to_end("mobilenet_v2", 32)
+
+
+def test_mobilenet_v2_within_fp32_orders():
+    import conditioning as C
+    _check_within_fp32_orders("mobilenet_v2", C.ENSEMBLE)
 
 
 @pytest.mark.parametrize("batch", [1, 4, 16, 64])

@@ -25,7 +25,7 @@ def make(in_chw, specs):
 
 
 def check(m, dtype, batch, begin=0, end=None, seed=0, kind="normal", in_chw=None, tol=None,
-          exact=False):
+          exact=False, tuning=None):
     from paper_2507_18748_amd import Partition
     end = len(m.layers) if end is None else end
     P = W.model_params(m, seed, dtype, begin, end)
@@ -34,7 +34,8 @@ def check(m, dtype, batch, begin=0, end=None, seed=0, kind="normal", in_chw=None
     print(f"[layer-parity] {[L.name for L in m.layers[begin:end]]} dtype={dtype} batch={batch}",
           flush=True)
     ref = oracle.forward(m.layers, P, begin, end, x, dtype)
-    with Partition(m.layers, P, (m.in_c, m.in_h, m.in_w), begin, end, dtype, max_batch=batch) as part:
+    with Partition(m.layers, P, (m.in_c, m.in_h, m.in_w), begin, end, dtype, max_batch=batch,
+                   tuning=tuning) as part:
         got = gpu_forward(part, x)
     got = got.reshape(ref.shape)
     if exact:
@@ -73,18 +74,20 @@ PW_CASES = [
 
 @pytest.mark.parametrize("dtype", ["f16", "bf16"])
 @pytest.mark.parametrize("ci,co,h,w,batch,res,act", PW_CASES)
-def test_pointwise_kernel(monkeypatch, dtype, ci, co, h, w, batch, res, act):
+def test_pointwise_kernel(dtype, ci, co, h, w, batch, res, act):
     from paper_2507_18748_amd import Partition
-    monkeypatch.setenv("PPIPE_GEMM_PLAN", "17")
+    tuning = {"gemm_plan": (17,)}
     if res:   # residual source: a 3x3 convolution of the same input
         specs = [conv("r", -1, ci, co, 3, 1, 1), conv("c", -1, ci, co, act=act, res=0)]
     else:
         specs = [conv("c", -1, ci, co, act=act)]
     m = make((ci, h, w), specs)
     with Partition(m.layers, W.model_params(m, 0, dtype), (ci, h, w), 0, len(specs), dtype,
-                   max_batch=batch) as part:
-        assert part.layer_info(len(specs) - 1, batch)["kernel"].startswith("pw_conv<")
-    check(m, dtype, batch)
+                   max_batch=batch, tuning=tuning) as part:
+        li = part.layer_info(len(specs) - 1, batch)
+        assert li["kernel"].startswith("pw_conv<") and li["forced"] == 1
+        assert part.info["tuned"] == 1
+    check(m, dtype, batch, tuning=tuning)
 
 
 # Stems: (C, Co, k, stride, pad, H, W, batch) of images with C <= 4 channels.
@@ -117,7 +120,7 @@ def test_stem_kernel_four_channels():
 
 
 @pytest.mark.parametrize("grid", ["1", "8"])
-def test_pointwise_grid_stride_matches_default(monkeypatch, grid):
+def test_pointwise_grid_stride_matches_default(grid):
     """A pointwise launch capped at 1 or 8 blocks (every wave walks many
     16-pixel groups with loads in flight ahead) gives the default's bits."""
     from paper_2507_18748_amd import Partition
@@ -125,11 +128,12 @@ def test_pointwise_grid_stride_matches_default(monkeypatch, grid):
     P = W.model_params(m, 0, "bf16")
     x = W.partition_input((24, 37, 29), 3, 5, "bf16", "normal")
     outs = []
-    monkeypatch.setenv("PPIPE_GEMM_PLAN", "17")
     for g in (None, grid):
+        tuning = {"gemm_plan": (17,)}
         if g:
-            monkeypatch.setenv("PPIPE_PW_GRID", g)
-        with Partition(m.layers, P, (24, 37, 29), 0, 1, "bf16", max_batch=3) as part:
+            tuning["stream_grid"] = int(g)
+        with Partition(m.layers, P, (24, 37, 29), 0, 1, "bf16", max_batch=3,
+                       tuning=tuning) as part:
             assert part.layer_info(0, 3)["kernel"].startswith("pw_conv<")
             outs.append(gpu_forward(part, x))
     np.testing.assert_array_equal(outs[0], outs[1])
@@ -302,21 +306,21 @@ FORCED_SHAPES = {  # ragged M and Co, padded 3x3 taps, a 1x1 with a K tail, an F
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("shape", list(FORCED_SHAPES))
 @pytest.mark.parametrize("plan,family,tile", FORCED)
-def test_forced_gemm_configuration(monkeypatch, plan, family, tile, shape, dtype):
+def test_forced_gemm_configuration(plan, family, tile, shape, dtype):
     """Every tile configuration, wave count and split count against the oracle
     (forced through the planner override)."""
     from paper_2507_18748_amd import Partition
     in_chw, specs, batch, kind = FORCED_SHAPES[shape]
     if shape == "stem" and family == "conv_gemm_skinny<":
         pytest.skip("the skinny kernel has no per-vector-tap gather")
-    monkeypatch.setenv("PPIPE_GEMM_PLAN", plan)
+    tuning = {"gemm_plan": tuple(int(v) for v in plan.split(","))}
     m = make(in_chw, specs)
     with Partition(m.layers, W.model_params(m, 0, dtype), in_chw, 0, 1, dtype,
-                   max_batch=batch) as part:
+                   max_batch=batch, tuning=tuning) as part:
         k = part.layer_info(0, batch)["kernel"]
     assert k.startswith(family) and tile in k, (plan, k)
     tol = {"f32": 1e-5, "bf16": 2.0 ** -7}[dtype] if shape != "fc" else 2e-2
-    check(m, dtype, batch, kind=kind, tol=tol)
+    check(m, dtype, batch, kind=kind, tol=tol, tuning=tuning)
 
 
 # A residual stage's first bottleneck: conv1 and the downsample projection read
@@ -379,3 +383,21 @@ def test_paired_downsample_launch(dtype, ci, mid, co, hw, s, batch):
     assert rel_inf(got, ref) <= LAYER_TOL[dtype]
     if dtype != "f32":
         assert paired, (k0, k2)
+
+
+def test_no_pairing_when_the_later_layer_adds_the_earlier_one():
+    """y = conv_b(x) + conv_a(x): conv_b reads conv_a's output as its residual,
+    so the two must not run as one launch at conv_a's position; the layer info
+    shows no pairing and the output matches the oracle."""
+    from paper_2507_18748_amd import Partition
+    ci, co, hw, batch = 128, 256, 7, 4
+    m = make((ci, hw, hw), [
+        conv("a", -1, ci, co, act="none"),
+        conv("b", -1, ci, co, act="relu", res=0),
+        dict(name="pool", op="gap", src=1, c_in=co, c_out=co),
+    ])
+    P = W.model_params(m, 1, "bf16")
+    with Partition(m.layers, P, (ci, hw, hw), 0, 3, "bf16", max_batch=batch) as part:
+        for i in (0, 1):
+            assert "paired=" not in part.layer_info(i, batch)["kernel"]
+    check(m, "bf16", batch, seed=1, kind="relu_normal")

@@ -137,7 +137,7 @@ def test_chained_blocks_match_the_whole_range_bitwise():
     np.testing.assert_array_equal(got.reshape(ref.shape), ref)
 
 
-@pytest.mark.parametrize("parts", [2, 3])
+@pytest.mark.parametrize("parts", [1, 2, 3, 4])
 def test_runs_on_cu_share_streams_match_the_default_stream(parts):
     """Virtual GPUs: each share's stream runs its own handle side by side
     with the others and gives the same bits as a run on the default stream."""
