@@ -181,6 +181,27 @@ ppipe_partition* ppipe_partition_create_tuned(const ppipe_model_desc* desc,
 int ppipe_partition_run(ppipe_partition* h, int32_t batch, const void* in,
                         void* out, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, allocation-free serving loops, harnesses that forbid hipMalloc):
+ * ppipe_partition_run with the kernels' scratch memory -- split-K partial
+ * sums, the fp32 logits of a final FC + softmax and the channel-padded input
+ * of a stem -- taken from a fixed device array of PPIPE_STATIC_SCRATCH_BYTES
+ * that the library holds on every device it runs on (from the first create
+ * on that device until the process ends), instead of the handle's
+ * workspace.  Intermediate activations stay in the handle's buffers, which
+ * create allocated.  Launches directly (a graph captured for the handle is
+ * not replayed); allocates nothing, no host synchronisation.  Same arguments
+ * and layouts as ppipe_partition_run and bit-identical output.  Returns
+ * PPIPE_E_INVALID, launching nothing, when the handle at `batch` needs more
+ * scratch than PPIPE_STATIC_SCRATCH_BYTES, PPIPE_E_HIP when the array's
+ * address could not be resolved on the handle's device.  Every call on one
+ * device shares that device's array and leaves its contents behind: calls
+ * whose work overlaps in time on one device (different streams, threads or
+ * handles) race on it. */
+#define PPIPE_STATIC_SCRATCH_BYTES ((int64_t)64 << 20)
+int ppipe_partition_run_static_scratch(ppipe_partition* h, int32_t batch, const void* in,
+                                       void* out, void* stream);
+
 /* Record the launches run() would issue for (batch, in, out) into a HIP
  * graph (host-side work only; allocates graph objects).  Later runs with the
  * same triple replay it.  Returns a status. */

@@ -142,6 +142,8 @@ def load_library() -> ctypes.CDLL:
                                                  ctypes.POINTER(Tuning)]
     lib.ppipe_partition_run.restype = ctypes.c_int
     lib.ppipe_partition_run.argtypes = [vp, i32, vp, vp, vp]
+    lib.ppipe_partition_run_static_scratch.restype = ctypes.c_int
+    lib.ppipe_partition_run_static_scratch.argtypes = [vp, i32, vp, vp, vp]
     lib.ppipe_partition_capture.restype = ctypes.c_int
     lib.ppipe_partition_capture.argtypes = [vp, i32, vp, vp]
     lib.ppipe_profile_layers.restype = ctypes.c_int
@@ -454,6 +456,12 @@ class Partition:
     def run(self, batch: int, x_ptr: int, out_ptr: int, stream: int = 0):
         """x_ptr / out_ptr: device addresses (tensor.data_ptr()); stream: hipStream_t."""
         self._check(self._lib.ppipe_partition_run(self._h, batch, x_ptr, out_ptr, stream))
+
+    def run_static_scratch(self, batch: int, x_ptr: int, out_ptr: int, stream: int = 0):
+        """run() with the kernels' scratch in the library's fixed per-device
+        array (allocates nothing; overlapping calls on one device race)."""
+        self._check(self._lib.ppipe_partition_run_static_scratch(self._h, batch, x_ptr,
+                                                                 out_ptr, stream))
 
     def capture(self, batch: int, x_ptr: int, out_ptr: int):
         self._check(self._lib.ppipe_partition_capture(self._h, batch, x_ptr, out_ptr))

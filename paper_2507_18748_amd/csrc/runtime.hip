@@ -20,6 +20,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -102,6 +103,13 @@ struct Plan {
 
 struct Shape {
     int c, h, w;
+};
+
+// Scratch memory of a run: split-K partial sums followed by the fp32 logits
+// of a final FC + softmax (ws), and the channel-padded input of a stem (pad).
+struct Workspace {
+    float* ws;
+    void* pad;
 };
 
 }  // namespace
@@ -427,7 +435,7 @@ void launch_work(const ppipe_partition* P, const LayerRT& l, int batch, int laun
 
 // GEMM arguments of layer l at a batch (x: the layer's input as the GEMM reads it).
 ConvGemmArgs gemm_args(const ppipe_partition* P, const LayerRT& l, int batch, const void* x,
-                       const void* res, void* y, bool padded)
+                       const void* res, void* y, bool padded, const Workspace& W)
 {
     const Plan& p = l.plans[batch - 1];
     ConvGemmArgs a;
@@ -438,8 +446,8 @@ ConvGemmArgs gemm_args(const ppipe_partition* P, const LayerRT& l, int batch, co
     a.res = res;
     a.y = y;
     a.M = batch * l.Ho * l.Wo;
-    a.partial = P->ws;
-    a.logits = P->ws + (p.splits > 1 ? (size_t)p.splits * a.M * l.Co : 0);
+    a.partial = W.ws;
+    a.logits = W.ws + (p.splits > 1 ? (size_t)p.splits * a.M * l.Co : 0);
     a.N = batch;
     a.H = l.H; a.W = l.W; a.C = padded ? l.cpad : l.C;
     a.Ho = l.Ho; a.Wo = l.Wo; a.Co = l.Co;
@@ -474,9 +482,13 @@ bool pair_runs(const ppipe_partition* P, const LayerRT& a, const LayerRT& b, int
 }
 
 // Enqueue the launches of one layer; only >= 0 restricts to that launch.
+Workspace handle_workspace(const ppipe_partition* P) { return Workspace{P->ws, P->pad_buf}; }
+
 hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, const void* in,
-                         void* out, hipStream_t s, LaunchHook* hook, int only = -1)
+                         void* out, hipStream_t s, LaunchHook* hook, int only = -1,
+                         const Workspace* wsp = nullptr)
 {
+    const Workspace W = wsp ? *wsp : handle_workspace(P);
     const void* x = buf_ptr(P, l.in_buf, in, out);
     void* y = const_cast<void*>(buf_ptr(P, l.out_buf, in, out));
     const void* res = buf_ptr(P, l.res_buf, in, out);
@@ -491,7 +503,7 @@ hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, 
         if (pad) {
             if (want(li)) {
                 if (hook) hook->before(l, li, s);
-                e = launch_pad_channels(P->dtype, x, P->pad_buf, (size_t)batch * l.H * l.W, l.C,
+                e = launch_pad_channels(P->dtype, x, W.pad, (size_t)batch * l.H * l.W, l.C,
                                         l.cpad, s);
                 if (hook) hook->after(l, li, s);
                 if (e != hipSuccess) return e;
@@ -499,7 +511,7 @@ hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, 
             ++li;
         }
         const ConvGemmArgs a =
-            gemm_args(P, l, batch, pad ? (const void*)P->pad_buf : x, res, y, pad);
+            gemm_args(P, l, batch, pad ? (const void*)W.pad : x, res, y, pad, W);
         if (want(li)) {
             if (hook) hook->before(l, li, s);
             e = launch_conv_gemm(P->dtype, p.cfg, p.wk, tapv_of(l, p), a, s);
@@ -552,8 +564,9 @@ hipError_t enqueue_layer(const ppipe_partition* P, const LayerRT& l, int batch, 
 // lead's position; runs with a hook (per-layer and per-launch timing) keep
 // one launch sequence per layer.
 hipError_t enqueue_all(const ppipe_partition* P, int batch, const void* in, void* out,
-                       hipStream_t s, LaunchHook* hook)
+                       hipStream_t s, LaunchHook* hook, const Workspace* wsp = nullptr)
 {
+    const Workspace W = wsp ? *wsp : handle_workspace(P);
     for (const LayerRT& l : P->L) {
         hipError_t e;
         if (!hook && l.pair >= 0 && pair_runs(P, l.pair_lead ? l : P->L[l.pair],
@@ -564,14 +577,14 @@ hipError_t enqueue_all(const ppipe_partition* P, int batch, const void* in, void
             const ConvGemmArgs a0 = gemm_args(P, l, batch, buf_ptr(P, l.in_buf, in, out),
                                               buf_ptr(P, l.res_buf, in, out),
                                               const_cast<void*>(buf_ptr(P, l.out_buf, in, out)),
-                                              false);
+                                              false, W);
             const ConvGemmArgs a1 = gemm_args(P, m, batch, buf_ptr(P, m.in_buf, in, out),
                                               buf_ptr(P, m.res_buf, in, out),
                                               const_cast<void*>(buf_ptr(P, m.out_buf, in, out)),
-                                              false);
+                                              false, W);
             e = launch_conv_gemm_pair(P->dtype, l.plans[batch - 1].cfg, a0, a1, s);
         } else {
-            e = enqueue_layer(P, l, batch, in, out, s, hook);
+            e = enqueue_layer(P, l, batch, in, out, s, hook, -1, &W);
         }
         if (e != hipSuccess)
             return e;
@@ -1123,6 +1136,55 @@ hipError_t time_reps(hipStream_t s, Events& ev, int reps, F&& enqueue, std::vect
     us.push_back(ms * 1000.0f / (float)reps);
     return e;
 }
+// ---- fixed scratch memory of ppipe_partition_run_static_scratch ----
+// One copy per device, allocated with the code object and held until the
+// process ends.  Host code must not use the array's name as a device address
+// (on the host it is only a stand-in): the device address comes from
+// hipGetSymbolAddress, resolved once per device with that device current.
+static __device__ __align__(256) unsigned char scratch[PPIPE_STATIC_SCRATCH_BYTES];
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES] = {};
+hipError_t g_scratch_err[MAX_DEVICES] = {};
+bool g_scratch_done[MAX_DEVICES] = {};
+
+// Resolves the scratch array's address on the current device (once).
+void resolve_scratch(int dev)
+{
+    if (dev < 0 || dev >= MAX_DEVICES) return;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (g_scratch_done[dev]) return;
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    g_scratch_err[dev] = e;
+    g_scratch_ptr[dev] = e == hipSuccess ? ptr : nullptr;
+    g_scratch_done[dev] = true;
+}
+
+size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+// Scratch bytes a run at `batch` needs: split-K partials and logits (the
+// largest over the layers, each layer reuses the region), then the padded
+// stem input.
+void scratch_need(const ppipe_partition* P, int batch, size_t* ws_bytes, size_t* pad_bytes)
+{
+    size_t ws = 0, pad = 0;
+    const int esz = dtype_size(P->dtype);
+    for (const LayerRT& l : P->L) {
+        if (l.kind != K_GEMM) continue;
+        const Plan& p = l.plans[batch - 1];
+        const size_t M = (size_t)batch * l.Ho * l.Wo;
+        size_t n = 0;
+        if (p.splits > 1) n += (size_t)p.splits * M * l.Co;
+        if (l.softmax) n += M * l.Co;
+        ws = std::max(ws, n * sizeof(float));
+        if (pads_input(l, p)) pad = std::max(pad, (size_t)batch * l.H * l.W * l.cpad * esz);
+    }
+    *ws_bytes = ws;
+    *pad_bytes = pad;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1190,6 +1252,10 @@ ppipe_partition* ppipe_partition_create_tuned(const ppipe_model_desc* desc,
         g_status = st;
         return nullptr;
     }
+    // set-up of the fixed scratch memory on this device (its address is
+    // looked up once per device; ppipe_partition_run_static_scratch reports
+    // a failure)
+    resolve_scratch(P->device);
     return P;
 }
 
@@ -1219,6 +1285,40 @@ int ppipe_partition_run(ppipe_partition* h, int32_t batch, const void* in, void*
         }
     }
     hipError_t e = enqueue_all(h, batch, in, out, s, nullptr);
+    if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("kernel launch", e));
+    return PPIPE_OK;
+}
+
+int ppipe_partition_run_static_scratch(ppipe_partition* h, int32_t batch, const void* in,
+                                       void* out, void* stream)
+{
+    int rc = check_run_args(h, batch, in, out);
+    if (rc != PPIPE_OK) return rc;
+    if ((rc = ensure_device(h)) != PPIPE_OK) return rc;
+    size_t ws = 0, pad = 0;
+    scratch_need(h, batch, &ws, &pad);
+    if (align256(ws) + pad > (size_t)PPIPE_STATIC_SCRATCH_BYTES)
+        return fail(PPIPE_E_INVALID,
+                    "batch " + std::to_string(batch) + " needs " +
+                        std::to_string(align256(ws) + pad) + " bytes of scratch, more than the " +
+                        std::to_string((long long)PPIPE_STATIC_SCRATCH_BYTES) + " held");
+    const int dev = h->device;
+    if (dev < 0 || dev >= MAX_DEVICES)
+        return fail(PPIPE_E_INVALID, "device index beyond the scratch table");
+    void* base = nullptr;
+    {
+        std::lock_guard<std::mutex> lk(g_scratch_mu);
+        if (!g_scratch_done[dev] || g_scratch_err[dev] != hipSuccess || !g_scratch_ptr[dev])
+            return fail(PPIPE_E_HIP, hip_msg("scratch address (hipGetSymbolAddress)",
+                                             g_scratch_done[dev] ? g_scratch_err[dev]
+                                                                 : hipErrorNotInitialized));
+        base = g_scratch_ptr[dev];
+    }
+    // every scratch byte a kernel reads was written earlier in the same run
+    // (split partials by the GEMM, logits by the GEMM, the padded input by
+    // the pad kernel), so nothing needs clearing
+    const Workspace W{ws ? (float*)base : nullptr, pad ? (uint8_t*)base + align256(ws) : nullptr};
+    hipError_t e = enqueue_all(h, batch, in, out, (hipStream_t)stream, nullptr, &W);
     if (e != hipSuccess) return fail(PPIPE_E_HIP, hip_msg("kernel launch", e));
     return PPIPE_OK;
 }
