@@ -32,6 +32,7 @@
 //    connected layers) use a second kernel, see conv_gemm_skinny below.
 #include "kernels.h"
 
+#include <mutex>
 #include <type_traits>
 
 namespace ppipe {
@@ -553,6 +554,88 @@ __device__ __forceinline__ void dma_wait()
     asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
 }
 
+
+// ---- prefetched single-pass epilogue (LDS-staged kernels) ----------------
+// Dynamic LDS of a staged kernel: the stage ring, or the whole fp32
+// [pixel][channel] accumulator tile (rows padded by 4 floats) when that is
+// larger, so the epilogue stages the tile in one pass.
+constexpr int gemm_lds_bytes(int BM, int BN, int NS)
+{
+    return NS * (BM + BN) * 128 > BN * (BM + 4) * 4 ? NS * (BM + BN) * 128 : BN * (BM + 4) * 4;
+}
+
+// Epilogue operands of one thread.  A thread finishes the same EPV channels
+// (co0 + c, c fixed by the thread index) of NV pixel rows of the tile, so its
+// scale, shift and residual vectors are all known when the K loop ends: their
+// loads go out together, before the tile is staged, instead of one dependent
+// chain per pass.
+template <typename T, int BM, int BN, int NT>
+struct EpiPre {
+    static constexpr int ESZ = (int)sizeof(T);
+    static constexpr int EPV = 16 / ESZ;
+    static constexpr int VPR = BM / EPV;          // 16-byte vectors per staged pixel row
+    static constexpr int NV = BN * VPR / NT;      // vectors per thread
+    static_assert(NT % VPR == 0 && (BN * VPR) % NT == 0, "fixed channel group per thread");
+    floatx4 sc[EPV / 4], bi[EPV / 4];
+    uint4 res[NV];
+
+    __device__ __forceinline__ void load(const ConvGemmArgs& a, int m0, int co0, int tid)
+    {
+        const int co = co0 + (tid % VPR) * EPV;
+        const bool cok = co < a.Co;                // Co % EPV == 0: the whole vector is in range
+        const auto sr = make_rsrc(a.scale, (uint32_t)a.Co * 4);
+        const auto br = make_rsrc(a.bias, (uint32_t)a.Co * 4);
+#pragma unroll
+        for (int q = 0; q < EPV / 4; ++q) {
+            sc[q] = __builtin_bit_cast(floatx4, buf_load16(sr, cok ? (uint32_t)(co + 4 * q) * 4 : OOB));
+            bi[q] = __builtin_bit_cast(floatx4, buf_load16(br, cok ? (uint32_t)(co + 4 * q) * 4 : OOB));
+        }
+        if (a.res) {
+            const auto rr = make_rsrc(a.res, (uint32_t)((size_t)a.M * a.Co * ESZ));
+#pragma unroll
+            for (int k = 0; k < NV; ++k) {
+                const int m = m0 + (tid + k * NT) / VPR;
+                res[k] = buf_load16(rr, cok && m < a.M ? (uint32_t)(((size_t)m * a.Co + co) * ESZ) : OOB);
+            }
+        }
+    }
+
+    // The tile is staged in ep ([pixel][channel] fp32, LROW floats a row).
+    template <int LROW>
+    __device__ __forceinline__ void finish(const ConvGemmArgs& a, const float* ep, int m0, int co0,
+                                           int tid) const
+    {
+        const int c = (tid % VPR) * EPV, co = co0 + c;
+        if (co >= a.Co)
+            return;
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            const int row = (tid + k * NT) / VPR, m = m0 + row;
+            if (m >= a.M)
+                break;                            // rows grow with k
+            float o[EPV];
+#pragma unroll
+            for (int q = 0; q < EPV / 4; ++q) {
+                const floatx4 x = *(const floatx4*)(ep + row * LROW + c + 4 * q);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) o[4 * q + j] = x[j] * sc[q][j] + bi[q][j];
+            }
+            if (a.res) {
+                T r[EPV];
+                __builtin_memcpy(r, &res[k], 16);
+#pragma unroll
+                for (int j = 0; j < EPV; ++j) o[j] += (float)r[j];
+            }
+            T e[EPV];
+#pragma unroll
+            for (int j = 0; j < EPV; ++j) e[j] = (T)apply_act(o[j], a.act);
+            uint4 u;
+            __builtin_memcpy(&u, e, 16);
+            *(uint4*)((T*)a.y + (size_t)m * a.Co + co) = u;
+        }
+    }
+};
+
 template <typename T, int BM, int BN, int WM, int WN, int NS, bool TAPV>
 __device__ __forceinline__ void conv_gemm_dma_body(const ConvGemmArgs& a, int bid, int G)
 {
@@ -586,6 +669,9 @@ __device__ __forceinline__ void conv_gemm_dma_body(const ConvGemmArgs& a, int bi
     const int nst = kc_end - kc_begin;
     const auto wsrc = make_rsrc(a.w, (uint32_t)a.Co * a.Kpad * ESZ);
     const auto xsrc = make_rsrc(a.x, (uint32_t)a.N * a.H * a.W * a.C * ESZ);
+    // plain tiles (no K split, no softmax logits, whole 16-byte channel
+    // vectors) take the one-pass epilogue
+    const bool fast_epi = a.splits == 1 && !a.softmax && a.Co % EPV == 0;
 
     if constexpr (TAPV) {
         for (int q = tid; q < a.Kpad / EPV && q < GEMM_VTAB_MAX; q += NW * 64) {
@@ -774,9 +860,27 @@ __device__ __forceinline__ void conv_gemm_dma_body(const ConvGemmArgs& a, int bi
     // The accumulators go to a [pixel][channel] fp32 tile in the (now idle)
     // stage ring, then each thread finishes VE consecutive channels of one
     // pixel: scale, bias, residual and activation read and write whole
-    // 16-byte vectors along the NHWC rows.  Tiles larger than the ring are
-    // staged in passes of CH pixel rows (whole wave columns).
+    // 16-byte vectors along the NHWC rows.  Plain tiles are staged in one
+    // pass (the launch provides LDS for the whole tile), their operand loads
+    // issued before the staging; split-K partials, softmax logits and ragged
+    // channel vectors take passes of CH pixel rows.
     constexpr int LROW = BM + 4;   // floats per staged pixel row (padding spreads banks)
+    if (fast_epi) {
+        // the epilogue's loads go out first and land while the tile is staged
+        EpiPre<T, BM, BN, NW * 64> epre;
+        epre.load(a, m0, co0, tid);
+        float* ept = (float*)dyn_smem;
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+                *(floatx4*)(ept + (wn * WTN + j * 16 + (lane & 15)) * LROW + wm * WTM + i * 16 +
+                            4 * (lane >> 4)) = acc[i][j];
+        __syncthreads();
+        epre.template finish<LROW>(a, ept, m0, co0, tid);
+        return;
+    }
     constexpr int CH0 = NS * STAGE / (LROW * 4);
     constexpr int CH = CH0 >= BN ? BN : CH0 / WTN * WTN;
     static_assert(CH >= WTN, "the ring holds at least one wave column of the tile");
@@ -824,6 +928,296 @@ conv_gemm_dma_pair(ConvGemmPair p)
     const int q = bid < p.n0 ? 0 : 1;   // block-uniform: one inlined body
     conv_gemm_dma_body<T, BM, BN, WM, WN, NS, false>(p.a[q], q ? bid - p.n0 : bid,
                                                       q ? (int)gridDim.x - p.n0 : p.n0);
+}
+
+// ---- 32x32 matrix-instruction variant -------------------------------------
+// Same LDS-direct operand staging, tile map and epilogue as conv_gemm_dma,
+// but each wave owns a 64x64 (or larger) tile computed with
+// v_mfma_f32_32x32x16_{f16,bf16}.  A wave tile of 64x64 reads 4 KB of
+// fragments per 16-deep k-step for four 32-cycle products (32 B per clock per
+// SIMD), a third less LDS read traffic per FLOP than the 64x32 wave tile of
+// the 16x16 kernel.  Fragments are double-buffered per k-step: the reads of
+// k-step t + 1 are in flight while the products of k-step t run, and the
+// first reads of the next stage go out right after its barrier, before the
+// last products of the current stage.
+//
+// Fragment layout of the 32x32x16 instruction (both operands): lane L
+// supplies row L % 32 of its 32-row slice and the 8 consecutive k of half
+// L / 32 of the 16-deep step, one 16-byte LDS read.  The accumulator of lane
+// L holds column (pixel) L % 32 and rows (channels) 8q + 4 (L / 32) + r in
+// element 4q + r.
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+template <typename T> struct Mfma32;
+template <> struct Mfma32<_Float16> {
+    static __device__ __forceinline__ void step(const uint4& a, const uint4& b, floatx16& c)
+    {
+        c = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(halfx8, a),
+                                                   __builtin_bit_cast(halfx8, b), c, 0, 0, 0);
+    }
+};
+template <> struct Mfma32<__bf16> {
+    static __device__ __forceinline__ void step(const uint4& a, const uint4& b, floatx16& c)
+    {
+        c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+    }
+};
+
+// Wait until this wave's LDS reads have all returned.
+__device__ __forceinline__ void lds_wait_all() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// Stage-row swizzle of the 32x32 layout: vector kv of row r sits at slot
+// kv ^ mx_swz(r).  A 32x32x16 fragment read takes 32 consecutive rows at two
+// slots; with kv ^ (r & 7) alone, rows r and r + 8 collide (two-way bank
+// conflicts on every read, measured with SQ_LDS_BANK_CONFLICT: 4 of the 8
+// cycles of a 1 KB read), and flipping bit 0 for rows 8..15 of every 16
+// removes them (a conflict-free 16-byte read of 64 lanes takes 4 cycles).
+__device__ __forceinline__ int mx_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+template <typename T, int BM, int BN, int WM, int WN, int NS, bool TAPV>
+__device__ __forceinline__ void conv_gemm_mx_body(const ConvGemmArgs& a, int bid, int G)
+{
+    static_assert(sizeof(T) == 2, "16-bit operands only");
+    constexpr int NW = WM * WN;
+    constexpr int ESZ = 2;
+    constexpr int EPV = 8;
+    constexpr int KV = 8;                      // 16-byte vectors of K per row per stage
+    constexpr int BK = KV * EPV;               // 64 K elements per stage
+    constexpr int ROW = KV * 16;
+    constexpr int STAGE = (BM + BN) * ROW;
+    constexpr int WTM = BM / WM, WTN = BN / WN;
+    constexpr int FM = WTM / 32, FN = WTN / 32;
+    constexpr int KS = KV / 2;                 // 16-deep k-steps per stage
+    constexpr int PER_A = BM / (8 * NW), PER_B = BN / (8 * NW);
+    constexpr int PER = PER_A + PER_B;
+    static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "whole 8-row groups per wave");
+    static_assert(NS >= 2 && (NS - 2) * PER < 64, "ring depth");
+    static_assert(FM >= 1 && FN >= 1 && WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
+
+    extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
+    __shared__ int vtab[TAPV ? GEMM_VTAB_MAX : 1];
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)dyn_smem;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave % WM, wn = wave / WM;
+    const int3 tt = tile_of_block(a, bid, G);
+    const int m0 = tt.x * BN, co0 = tt.y * BM;
+    const int kc_begin = tt.z * a.chunks_per_split;
+    const int kc_end = min(a.total_chunks, kc_begin + a.chunks_per_split);
+    const int nst = kc_end - kc_begin;
+    const auto wsrc = make_rsrc(a.w, (uint32_t)a.Co * a.Kpad * ESZ);
+    const auto xsrc = make_rsrc(a.x, (uint32_t)a.N * a.H * a.W * a.C * ESZ);
+    // plain tiles (no K split, no softmax logits, whole 16-byte channel
+    // vectors) take the one-pass epilogue
+    const bool fast_epi = a.splits == 1 && !a.softmax && a.Co % EPV == 0;
+
+    if constexpr (TAPV) {
+        for (int q = tid; q < a.Kpad / EPV && q < GEMM_VTAB_MAX; q += NW * 64) {
+            int e = -1;
+            const int k = q * EPV;
+            if (k < a.K) {
+                const int tap = k / a.C, ci = k - tap * a.C;
+                const int kh = tap / a.KW, kw = tap - kh * a.KW;
+                e = kh | (kw << 8) | (ci << 16);
+            }
+            vtab[q] = e;
+        }
+        __syncthreads();
+    }
+
+    // load slots: load i of wave w fills rows 8 (i NW + w) .. + 8 of its
+    // operand; lane L covers row + L / 8, slot L % 8 (holding vector slot ^ mx_swz(row))
+    const int lr = lane >> 3, lp = lane & 7;
+    uint32_t a_off[PER_A];
+#pragma unroll
+    for (int i = 0; i < PER_A; ++i) {
+        const int row = 8 * (i * NW + wave) + lr;
+        const int kv = lp ^ mx_swz(row);
+        a_off[i] = co0 + row < a.Co ? (uint32_t)(((co0 + row) * a.Kpad + kv * EPV) * ESZ) : OOB;
+    }
+    PixelRow b_px[PER_B];
+    int b_k[PER_B];
+#pragma unroll
+    for (int i = 0; i < PER_B; ++i) {
+        const int row = 8 * (i * NW + wave) + lr;
+        b_px[i] = pixel_row(a, m0 + row, ESZ);
+        b_k[i] = lp ^ mx_swz(row);
+    }
+
+    TapCursor cur;
+    int lst = kc_begin;
+    cur.start(kc_begin * BK, a.C, a.KW);
+    auto issue = [&](uint32_t slot) {
+        const bool live = lst < kc_end;
+        const uint32_t k0b = (uint32_t)(lst * BK * ESZ);
+#pragma unroll
+        for (int i = 0; i < PER_A; ++i)
+            dma16(wsrc, live ? a_off[i] + k0b : OOB, slot + (i * NW + wave) * 8 * ROW);
+        const uint32_t bslot = slot + BM * ROW;
+        if constexpr (TAPV) {
+#pragma unroll
+            for (int i = 0; i < PER_B; ++i) {
+                const int e = live ? vtab[lst * KV + b_k[i]] : -1;
+                const int kh = e & 0xff, kw = (e >> 8) & 0xff, ci = e >> 16;
+                const bool ok = e >= 0 && ((b_px[i].hmask >> kh) & (b_px[i].wmask >> kw) & 1u);
+                dma16(xsrc, ok ? (uint32_t)(b_px[i].off + ((kh * a.W + kw) * a.C + ci) * ESZ) : OOB,
+                      bslot + (i * NW + wave) * 8 * ROW);
+            }
+        } else {
+            const int tap_off = ((cur.kh * a.W + cur.kw) * a.C + cur.ci) * ESZ;
+            const int cleft = a.C - cur.ci;
+#pragma unroll
+            for (int i = 0; i < PER_B; ++i) {
+                const bool ok = live &&
+                                ((b_px[i].hmask >> cur.kh) & (b_px[i].wmask >> cur.kw) & 1u) &&
+                                b_k[i] * EPV < cleft;
+                dma16(xsrc, ok ? (uint32_t)(b_px[i].off + tap_off + b_k[i] * 16) : OOB,
+                      bslot + (i * NW + wave) * 8 * ROW);
+            }
+        }
+        if (live) {
+            ++lst;
+            cur.advance(BK, a.C, a.KW);
+        }
+    };
+
+    floatx16 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+    // fragment offsets within a stage at k-step 0; k-step t reads offset ^ (t * 32)
+    // (rows of a fragment start at multiples of 32, so mx_swz(row) = mx_swz(lane % 32))
+    const int sw = ((lane >> 5) ^ mx_swz(lane & 31)) << 4;
+    int fa[FM], fb[FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) fa[i] = (wm * WTM + i * 32 + (lane & 31)) * ROW + sw;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) fb[j] = (BM + wn * WTN + j * 32 + (lane & 31)) * ROW + sw;
+
+    uint4 xa0[FM], xb0[FN], xa1[FM], xb1[FN];
+#define PPIPE_MXREAD(S, T_, XA, XB)                                                               \
+    do {                                                                                          \
+        _Pragma("unroll") for (int i = 0; i < FM; ++i)                                            \
+            XA[i] = *(const uint4*)((S) + (fa[i] ^ ((T_) << 5)));                                 \
+        _Pragma("unroll") for (int j = 0; j < FN; ++j)                                            \
+            XB[j] = *(const uint4*)((S) + (fb[j] ^ ((T_) << 5)));                                 \
+    } while (0)
+#define PPIPE_MXMMA(XA, XB)                                                                       \
+    do {                                                                                          \
+        _Pragma("unroll") for (int i = 0; i < FM; ++i)                                            \
+            _Pragma("unroll") for (int j = 0; j < FN; ++j)                                        \
+                Mfma32<T>::step(XA[i], XB[j], acc[i][j]);                                         \
+    } while (0)
+
+    if (nst > 0) {
+#pragma unroll
+        for (int p = 0; p < NS - 1; ++p)
+            issue(lds0 + p * STAGE);
+        dma_wait<(NS - 2) * PER>();    // stage 0 of this wave
+        bare_barrier();                // ... and of every wave
+        int rd = 0;                    // slot of stage s
+        PPIPE_MXREAD(dyn_smem, 0, xa0, xb0);
+        for (int s = 0; s < nst; ++s) {
+            // every wave finished reading stage s - 1 before the barrier above:
+            // its slot takes stage s + NS - 1
+            issue(lds0 + (rd == 0 ? NS - 1 : rd - 1) * STAGE);
+            const unsigned char* S = dyn_smem + rd * STAGE;
+#pragma unroll
+            for (int t = 0; t < KS; t += 2) {
+                PPIPE_MXREAD(S, t + 1, xa1, xb1);
+                PPIPE_MXMMA(xa0, xb0);
+                __builtin_amdgcn_sched_group_barrier(0x100, FM + FN, 0);   // reads of t + 1
+                __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);   // then products of t
+                if (t + 2 < KS) {
+                    PPIPE_MXREAD(S, t + 2, xa0, xb0);
+                    PPIPE_MXMMA(xa1, xb1);
+                    __builtin_amdgcn_sched_group_barrier(0x100, FM + FN, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
+                }
+            }
+            // last k-step of stage s: its fragments are in xa1/xb1.  All of
+            // this wave's reads of stage s have returned (lgkmcnt 0) and its
+            // loads of stage s + 1 have landed; after the barrier every wave's
+            // have, so stage s + 1's first fragments can be read while the
+            // last products of stage s run.
+            lds_wait_all();
+            if (s + 1 < nst) {
+                dma_wait<(NS - 2) * PER>();
+                bare_barrier();
+                rd = rd + 1 == NS ? 0 : rd + 1;
+                PPIPE_MXREAD(dyn_smem + rd * STAGE, 0, xa0, xb0);
+            }
+            PPIPE_MXMMA(xa1, xb1);
+        }
+        dma_wait<0>();   // the empty tail loads
+    }
+#undef PPIPE_MXMMA
+#undef PPIPE_MXREAD
+
+    // ---- epilogue staged through LDS: [pixel][channel] fp32 tile ----
+    constexpr int LROW = BM + 4;
+    if (fast_epi) {   // one pass, operands loaded first (as in conv_gemm_dma_body)
+        EpiPre<T, BM, BN, NW * 64> epre;
+        epre.load(a, m0, co0, tid);
+        float* ept = (float*)dyn_smem;
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const floatx4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1],
+                                       acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+                    *(floatx4*)(ept + (wn * WTN + j * 32 + (lane & 31)) * LROW + wm * WTM +
+                                i * 32 + 8 * q + 4 * (lane >> 5)) = v;
+                }
+        __syncthreads();
+        epre.template finish<LROW>(a, ept, m0, co0, tid);
+        return;
+    }
+    constexpr int CH0 = NS * STAGE / (LROW * 4);
+    constexpr int CH = CH0 >= BN ? BN : CH0 / WTN * WTN;
+    static_assert(CH >= WTN, "the ring holds at least one wave column of the tile");
+    float* ep = (float*)dyn_smem;
+#pragma unroll
+    for (int p0 = 0; p0 < BN; p0 += CH) {
+        __syncthreads();
+        const int wc = wn * WTN;
+        if (wc >= p0 && wc < p0 + CH) {
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+                for (int j = 0; j < FN; ++j)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const floatx4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1],
+                                           acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+                        *(floatx4*)(ep + (wc - p0 + j * 32 + (lane & 31)) * LROW + wm * WTM +
+                                    i * 32 + 8 * q + 4 * (lane >> 5)) = v;
+                    }
+        }
+        __syncthreads();
+        const int rows = min(CH, BN - p0);
+        if (a.Co % EPV == 0)
+            epi_rows<T, EPV, BM, LROW, NW * 64>(a, ep, rows, m0 + p0, co0, tt.z, tid);
+        else
+            epi_rows<T, 4, BM, LROW, NW * 64>(a, ep, rows, m0 + p0, co0, tt.z, tid);
+    }
+}
+
+template <typename T, int BM, int BN, int WM, int WN, int NS, bool TAPV>
+__global__ void __launch_bounds__(WM * WN * 64)
+conv_gemm_mx(ConvGemmArgs a)
+{
+    conv_gemm_mx_body<T, BM, BN, WM, WN, NS, TAPV>(a, (int)blockIdx.x, (int)gridDim.x);
 }
 
 // Split-K reduction: one thread per 4 output channels of one pixel, partials
@@ -1073,6 +1467,14 @@ GemmCfgInfo gemm_cfg_info(int cfg)
     case GEMM_DMA_64x64_8W_S6: return {64, 64, 8, false, 6, 8};
     case GEMM_DMA_64x128_8W_S2: return {64, 128, 8, false, 2, 8};
     case GEMM_DMA_64x256_8W_S2: return {64, 256, 8, false, 2, 8};
+    case GEMM_MX_128x128_S2: return {128, 128, 8, false, 2, 4, 32};
+    case GEMM_MX_128x128_S3: return {128, 128, 8, false, 3, 4, 32};
+    case GEMM_MX_128x128_S4: return {128, 128, 8, false, 4, 4, 32};
+    case GEMM_MX_256x128_S2: return {256, 128, 8, false, 2, 8, 32};
+    case GEMM_MX_128x256_S2: return {128, 256, 8, false, 2, 8, 32};
+    case GEMM_MX_256x128_S3: return {256, 128, 8, false, 3, 8, 32};
+    case GEMM_MX_128x128_8W_S2: return {128, 128, 8, false, 2, 8, 32};
+    case GEMM_MX_128x128_8W_S3: return {128, 128, 8, false, 3, 8, 32};
     default:            return {0, 0, 0, false};
     }
 }
@@ -1094,7 +1496,7 @@ static hipError_t launch_lds(bool tapv, const ConvGemmArgs& a, hipStream_t s)
 template <typename T, int BM, int BN, int WM, int WN, int NS, bool TAPV>
 static hipError_t launch_dma_one(const ConvGemmArgs& a, hipStream_t s)
 {
-    constexpr int bytes = NS * (BM + BN) * 128;
+    constexpr int bytes = gemm_lds_bytes(BM, BN, NS);
     static const hipError_t attr = hipFuncSetAttribute(
         (const void*)conv_gemm_dma<T, BM, BN, WM, WN, NS, TAPV>,
         hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
@@ -1109,7 +1511,7 @@ static hipError_t launch_dma_one(const ConvGemmArgs& a, hipStream_t s)
 template <typename T, int BM, int BN, int WM, int WN, int NS>
 static hipError_t launch_dma_pair(const ConvGemmArgs& a0, const ConvGemmArgs& a1, hipStream_t s)
 {
-    constexpr int bytes = NS * (BM + BN) * 128;
+    constexpr int bytes = gemm_lds_bytes(BM, BN, NS);
     static const hipError_t attr = hipFuncSetAttribute(
         (const void*)conv_gemm_dma_pair<T, BM, BN, WM, WN, NS>,
         hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
@@ -1123,6 +1525,32 @@ static hipError_t launch_dma_pair(const ConvGemmArgs& a0, const ConvGemmArgs& a1
     PPIPE_LAUNCH((conv_gemm_dma_pair<T, BM, BN, WM, WN, NS>), dim3((unsigned)(p.n0 + n1)),
                  dim3(WM * WN * 64), bytes, s, p);
     return hipGetLastError();
+}
+
+template <typename T, int BM, int BN, int WM, int WN, int NS, bool TAPV>
+static hipError_t launch_mx_one(const ConvGemmArgs& a, hipStream_t s)
+{
+    if constexpr (sizeof(T) != 2) {
+        return hipErrorInvalidValue;   // 32x32x16 instructions take 16-bit operands
+    } else {
+        constexpr int bytes = gemm_lds_bytes(BM, BN, NS);
+        static const hipError_t attr = hipFuncSetAttribute(
+            (const void*)conv_gemm_mx<T, BM, BN, WM, WN, NS, TAPV>,
+            hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+        if (attr != hipSuccess)
+            return attr;
+        PPIPE_LAUNCH((conv_gemm_mx<T, BM, BN, WM, WN, NS, TAPV>),
+                     dim3((unsigned)(a.tiles_m * a.tiles_co * a.splits)), dim3(WM * WN * 64),
+                     bytes, s, a);
+        return hipGetLastError();
+    }
+}
+
+template <typename T, int BM, int BN, int WM, int WN, int NS>
+static hipError_t launch_mx(bool tapv, const ConvGemmArgs& a, hipStream_t s)
+{
+    return tapv ? launch_mx_one<T, BM, BN, WM, WN, NS, true>(a, s)
+                : launch_mx_one<T, BM, BN, WM, WN, NS, false>(a, s);
 }
 
 template <typename T, int BM, int BN, int WM, int WN, int NS>
@@ -1181,6 +1609,14 @@ static hipError_t launch_cfg(int cfg, int wk, bool tapv, const ConvGemmArgs& a,
     case GEMM_DMA_64x64_8W_S6: return launch_dma<T, 64, 64, 2, 4, 6>(tapv, a, s);
     case GEMM_DMA_64x128_8W_S2: return launch_dma<T, 64, 128, 2, 4, 2>(tapv, a, s);
     case GEMM_DMA_64x256_8W_S2: return launch_dma<T, 64, 256, 2, 4, 2>(tapv, a, s);
+    case GEMM_MX_128x128_S2: return launch_mx<T, 128, 128, 2, 2, 2>(tapv, a, s);
+    case GEMM_MX_128x128_S3: return launch_mx<T, 128, 128, 2, 2, 3>(tapv, a, s);
+    case GEMM_MX_128x128_S4: return launch_mx<T, 128, 128, 2, 2, 4>(tapv, a, s);
+    case GEMM_MX_256x128_S2: return launch_mx<T, 256, 128, 4, 2, 2>(tapv, a, s);
+    case GEMM_MX_128x256_S2: return launch_mx<T, 128, 256, 2, 4, 2>(tapv, a, s);
+    case GEMM_MX_256x128_S3: return launch_mx<T, 256, 128, 4, 2, 3>(tapv, a, s);
+    case GEMM_MX_128x128_8W_S2: return launch_mx<T, 128, 128, 2, 4, 2>(tapv, a, s);
+    case GEMM_MX_128x128_8W_S3: return launch_mx<T, 128, 128, 2, 4, 3>(tapv, a, s);
     default:            return hipErrorInvalidValue;
     }
 }
@@ -1289,6 +1725,8 @@ static const char* dt_name(int dt)
 const char* conv_gemm_name(int dt, int cfg, int wk, bool tapv)
 {
     static char names[3][GEMM_NCFG][SKINNY_MAX_WAVES + 1][2][64];
+    static std::mutex mu;   // entries are written once, on first use, under the lock
+    std::lock_guard<std::mutex> lk(mu);
     const GemmCfgInfo c = gemm_cfg_info(cfg);
     const int w = c.skinny || cfg == GEMM_PW || cfg == GEMM_STEM ? wk : 0;
     char* n = names[dt][cfg][w][tapv ? 1 : 0];
@@ -1299,6 +1737,9 @@ const char* conv_gemm_name(int dt, int cfg, int wk, bool tapv)
             snprintf(n, 64, "stem_conv<%s,cf%d>", dt_name(dt), wk);
         else if (c.skinny)
             snprintf(n, 64, "conv_gemm_skinny<%s,%dx%d,waves%d>", dt_name(dt), c.bm, c.bn, wk);
+        else if (c.dma && c.mfma == 32)
+            snprintf(n, 64, "conv_gemm_mx<%s,%dx%d,%dw,dma%d%s>", dt_name(dt), c.bm, c.bn,
+                     c.waves, c.dma, tapv ? ",tapv" : "");
         else if (c.dma)
             snprintf(n, 64, "conv_gemm<%s,%dx%d,kv%d%s,dma%d%s>", dt_name(dt), c.bm, c.bn, c.kv,
                      c.waves == 8 ? ",8w" : "", c.dma, tapv ? ",tapv" : "");

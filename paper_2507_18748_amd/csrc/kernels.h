@@ -101,13 +101,24 @@ enum GemmCfg : int {
     GEMM_STEM = 18,
     GEMM_DMA_64x128_8W_S2 = 19,   // 8 waves, 32x32 per wave, 2 stages
     GEMM_DMA_64x256_8W_S2 = 20,   // 8 waves, 32 co x 64 m per wave, 2 stages
-    GEMM_NCFG = 21
+    // 32x32x16 matrix instructions (16-bit types only), 64x64 per wave,
+    // per-k-step double-buffered fragments, NS-stage LDS-direct ring
+    GEMM_MX_128x128_S2 = 21,      // 4 waves (2 x 2)
+    GEMM_MX_128x128_S3 = 22,
+    GEMM_MX_128x128_S4 = 23,
+    GEMM_MX_256x128_S2 = 24,      // 8 waves (4 x 2): 256 channels x 128 pixels
+    GEMM_MX_128x256_S2 = 25,      // 8 waves (2 x 4): 128 channels x 256 pixels
+    GEMM_MX_256x128_S3 = 26,
+    GEMM_MX_128x128_8W_S2 = 27,   // 8 waves (2 x 4): 64x32 per wave
+    GEMM_MX_128x128_8W_S3 = 28,
+    GEMM_NCFG = 29
 };
 struct GemmCfgInfo {
     int bm, bn, kv;       // tile rows (co), columns (m); kv: 16-byte vectors of K per LDS stage
     bool skinny;
     int dma = 0;          // LDS stages of the DMA-staged kernel (0: register-staged)
     int waves = 4;        // waves per block (LDS kernels)
+    int mfma = 16;        // 16: 16x16 matrix instructions; 32: 32x32x16 (16-bit types only)
 };
 GemmCfgInfo gemm_cfg_info(int cfg);
 // K elements per pipeline step: an LDS stage, or one 64-byte MFMA k-step (skinny)

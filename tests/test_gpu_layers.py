@@ -290,7 +290,17 @@ FORCED = [  # (configuration id, waves, splits): every kernel variant the planne
     ("16,0,1", "conv_gemm<", "64x64,kv8,8w,dma6"), ("16,0,2", "conv_gemm<", "64x64,kv8,8w,dma6"),
     ("19,0,1", "conv_gemm<", "64x128,kv8,8w,dma2"), ("19,0,2", "conv_gemm<", "64x128,kv8,8w,dma2"),
     ("20,0,1", "conv_gemm<", "64x256,kv8,8w,dma2"), ("20,0,3", "conv_gemm<", "64x256,kv8,8w,dma2"),
+    # 32x32x16 matrix instructions, 64x64 per wave (16-bit types only)
+    ("21,0,1", "conv_gemm_mx<", "128x128,4w,dma2"), ("21,0,3", "conv_gemm_mx<", "128x128,4w,dma2"),
+    ("22,0,1", "conv_gemm_mx<", "128x128,4w,dma3"), ("22,0,2", "conv_gemm_mx<", "128x128,4w,dma3"),
+    ("23,0,1", "conv_gemm_mx<", "128x128,4w,dma4"), ("23,0,3", "conv_gemm_mx<", "128x128,4w,dma4"),
+    ("24,0,1", "conv_gemm_mx<", "256x128,8w,dma2"), ("24,0,2", "conv_gemm_mx<", "256x128,8w,dma2"),
+    ("25,0,1", "conv_gemm_mx<", "128x256,8w,dma2"), ("25,0,3", "conv_gemm_mx<", "128x256,8w,dma2"),
+    ("26,0,1", "conv_gemm_mx<", "256x128,8w,dma3"), ("26,0,2", "conv_gemm_mx<", "256x128,8w,dma3"),
+    ("27,0,1", "conv_gemm_mx<", "128x128,8w,dma2"), ("27,0,3", "conv_gemm_mx<", "128x128,8w,dma2"),
+    ("28,0,1", "conv_gemm_mx<", "128x128,8w,dma3"), ("28,0,2", "conv_gemm_mx<", "128x128,8w,dma3"),
 ]
+MX_FORCED = [f for f in FORCED if f[1] == "conv_gemm_mx<"]
 FORCED_SHAPES = {  # ragged M and Co, padded 3x3 taps, a 1x1 with a K tail, an FC + softmax
     "3x3": ((64, 13, 13), [conv("c", -1, 64, 100, 3, 1, 1)], 3, "normal"),
     "1x1": ((24, 9, 9), [conv("c", -1, 24, 36, act="relu6")], 2, "normal"),
@@ -313,6 +323,8 @@ def test_forced_gemm_configuration(plan, family, tile, shape, dtype):
     in_chw, specs, batch, kind = FORCED_SHAPES[shape]
     if shape == "stem" and family == "conv_gemm_skinny<":
         pytest.skip("the skinny kernel has no per-vector-tap gather")
+    if family == "conv_gemm_mx<" and dtype == "f32":
+        pytest.skip("32x32x16 matrix instructions take 16-bit operands only")
     tuning = {"gemm_plan": tuple(int(v) for v in plan.split(","))}
     m = make(in_chw, specs)
     with Partition(m.layers, W.model_params(m, 0, dtype), in_chw, 0, 1, dtype,
@@ -401,3 +413,18 @@ def test_no_pairing_when_the_later_layer_adds_the_earlier_one():
         for i in (0, 1):
             assert "paired=" not in part.layer_info(i, batch)["kernel"]
     check(m, "bf16", batch, seed=1, kind="relu_normal")
+
+
+@pytest.mark.parametrize("shape", ["3x3", "3x3w", "stem"])
+@pytest.mark.parametrize("plan,family,tile", MX_FORCED)
+def test_forced_mx_configuration_f16(plan, family, tile, shape):
+    """The 32x32x16 configurations in fp16 (a separate instruction from bf16)."""
+    from paper_2507_18748_amd import Partition
+    in_chw, specs, batch, kind = FORCED_SHAPES[shape]
+    tuning = {"gemm_plan": tuple(int(v) for v in plan.split(","))}
+    m = make(in_chw, specs)
+    with Partition(m.layers, W.model_params(m, 0, "f16"), in_chw, 0, 1, "f16",
+                   max_batch=batch, tuning=tuning) as part:
+        k = part.layer_info(0, batch)["kernel"]
+    assert k.startswith(family) and tile in k, (plan, k)
+    check(m, "f16", batch, kind=kind, tuning=tuning)
