@@ -910,7 +910,8 @@ template <typename T, int BM, int BN, int WM, int WN, int NS, bool TAPV>
 __global__ void __launch_bounds__(WM * WN * 64)
 conv_gemm_dma(ConvGemmArgs a)
 {
-    conv_gemm_dma_body<T, BM, BN, WM, WN, NS, TAPV>(a, (int)blockIdx.x, (int)gridDim.x);
+    const int3 g = load_args_now(a, (int)blockIdx.x, (int)gridDim.x);
+    conv_gemm_dma_body<T, BM, BN, WM, WN, NS, TAPV>(a, g.x, g.y);
 }
 
 // Two independent layers of one tile configuration in one launch: blocks
@@ -1217,7 +1218,8 @@ template <typename T, int BM, int BN, int WM, int WN, int NS, bool TAPV>
 __global__ void __launch_bounds__(WM * WN * 64)
 conv_gemm_mx(ConvGemmArgs a)
 {
-    conv_gemm_mx_body<T, BM, BN, WM, WN, NS, TAPV>(a, (int)blockIdx.x, (int)gridDim.x);
+    const int3 g = load_args_now(a, (int)blockIdx.x, (int)gridDim.x);
+    conv_gemm_mx_body<T, BM, BN, WM, WN, NS, TAPV>(a, g.x, g.y);
 }
 
 // Split-K reduction: one thread per 4 output channels of one pixel, partials
@@ -1228,8 +1230,9 @@ conv_gemm_mx(ConvGemmArgs a)
 template <typename T>
 __global__ void __launch_bounds__(256) splitk_reduce_kernel(ConvGemmArgs a)
 {
+    const int3 g = load_args_now(a, (int)blockIdx.x, (int)gridDim.x);
     const uint32_t nvec = (uint32_t)a.M * a.Co / 4;
-    const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+    const uint32_t i = (uint32_t)g.x * 256u + threadIdx.x;
     if (i >= nvec)
         return;
     const auto src = make_rsrc(a.partial, (uint32_t)a.splits * nvec * 16u);
@@ -1274,7 +1277,8 @@ conv_gemm_skinny(ConvGemmArgs a)
     // wave-uniform: keeps the K-step and tap arithmetic on the scalar unit
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int g = lane >> 4, r = lane & 15;
-    const int3 tt = tile_of_block(a);
+    const int3 bg = load_args_now(a, (int)blockIdx.x, (int)gridDim.x);
+    const int3 tt = tile_of_block(a, bg.x, bg.y);
     const int m0 = tt.x * 16 * FN, co0 = tt.y * 16 * FM;
     const auto wsrc = make_rsrc(a.w, (uint32_t)a.Co * a.Kpad * ESZ);
     const auto xsrc = make_rsrc(a.x, (uint32_t)a.N * a.H * a.W * a.C * ESZ);

@@ -67,6 +67,26 @@ struct ConvGemmArgs {
     int grid_blocks;      // pointwise kernel: cap on blocks along the pixels (0: resident set)
 };
 
+// Bring every field of the kernel arguments into scalar registers at once.
+// Left to itself the compiler loads the argument struct in several batches,
+// each waited for before the next goes out; a kernel-argument read costs
+// ~0.25 us, so a GEMM block spent ~0.8 us before its first operand load.
+// One asm statement that names every field makes all loads go out together;
+// the block index passes through it, so no work that uses the arguments can
+// be scheduled before it (which would split the loads again), and so does
+// the grid size (a hidden kernel argument after the struct).
+__device__ __forceinline__ int3 load_args_now(const ConvGemmArgs& a, int bid, int grid,
+                                              int bid_y = 0)
+{
+    asm volatile("" : "+s"(bid), "+s"(grid), "+s"(bid_y) : "s"(a.x), "s"(a.w), "s"(a.scale), "s"(a.bias), "s"(a.res), "s"(a.y),
+                 "s"(a.logits), "s"(a.partial), "s"(a.N), "s"(a.H), "s"(a.W), "s"(a.C),
+                 "s"(a.Ho), "s"(a.Wo), "s"(a.Co), "s"(a.KH), "s"(a.KW), "s"(a.stride),
+                 "s"(a.pad), "s"(a.K), "s"(a.Kpad), "s"(a.M), "s"(a.act), "s"(a.total_chunks),
+                 "s"(a.splits), "s"(a.chunks_per_split), "s"(a.tiles_m), "s"(a.tiles_co),
+                 "s"(a.co_fastest), "s"(a.softmax), "s"(a.grid_blocks));
+    return make_int3(bid, grid, bid_y);
+}
+
 // Tile configurations (rows = co, columns = m).
 //   LDS-tiled kernel for large M: blocks of 4 waves share staged tiles.
 //   Skinny kernel for small M: a block of WK waves computes one small tile,

@@ -78,13 +78,18 @@ __device__ __forceinline__ uint4 dw_load(__amdgpu_buffer_rsrc_t r, uint32_t off)
 // hardware deals block b to XCD b % 8): neighbouring output rows, whose input
 // windows overlap, run on one XCD and share its L2 instead of each XCD
 // fetching the overlapping rows again.
-__device__ __forceinline__ uint32_t xcd_block()
+__device__ __forceinline__ uint32_t xcd_block(uint32_t b, uint32_t G)
 {
     constexpr uint32_t XCDS = 8;
-    const uint32_t G = gridDim.x, b = blockIdx.x;
     const uint32_t xcd = b % XCDS, slot = b / XCDS, per = G / XCDS, rem = G % XCDS;
     return xcd * per + (xcd < rem ? xcd : rem) + slot;
 }
+
+// Every kernel argument into scalar registers in one batch of loads (a
+// kernel-argument read costs ~0.25 us; left to itself the compiler issues
+// them in dependent batches), with the block index and grid size passed
+// through so that no argument-dependent work is scheduled before it.
+#define PPIPE_ARGS_NOW(B, G, ...) asm volatile("" : "+s"(B), "+s"(G) : __VA_ARGS__)
 
 template <typename T>
 __device__ __forceinline__ void unpack16(const uint4& u, float* f)
@@ -129,9 +134,12 @@ dwconv3_kernel(const T* __restrict__ x, const T* __restrict__ w, const float* __
     constexpr int NCOL = (PW - 1) * S + 3;     // input columns one row of PW outputs reads
     constexpr uint32_t OOB = 0x80000000u;
     const int CV = C / V;
+    uint32_t bid = blockIdx.x, grid = gridDim.x;
+    PPIPE_ARGS_NOW(bid, grid, "s"(x), "s"(w), "s"(scale), "s"(bias), "s"(y), "s"(N), "s"(H),
+                   "s"(W), "s"(C), "s"(Ho), "s"(Wo), "s"(pad), "s"(act));
     const int WQ = (Wo + PW - 1) / PW;
     const uint32_t total = (uint32_t)N * Ho * WQ * CV;
-    const uint32_t idx = xcd_block() * 256u + threadIdx.x;
+    const uint32_t idx = xcd_block(bid, grid) * 256u + threadIdx.x;
     if (idx >= total)
         return;
     const int cv = (int)(idx % CV);
@@ -238,8 +246,11 @@ maxpool_kernel(const T* __restrict__ x, T* __restrict__ y, int N, int H, int W, 
 {
     constexpr int V = Vec16<T>::N;
     const int CV = C / V;
+    uint32_t bid = blockIdx.x, grid = gridDim.x;
+    PPIPE_ARGS_NOW(bid, grid, "s"(x), "s"(y), "s"(N), "s"(H), "s"(W), "s"(C), "s"(Ho), "s"(Wo),
+                   "s"(k), "s"(stride), "s"(pad));
     const size_t total = (size_t)N * Ho * Wo * CV;
-    const size_t idx = (size_t)xcd_block() * blockDim.x + threadIdx.x;
+    const size_t idx = (size_t)xcd_block(bid, grid) * blockDim.x + threadIdx.x;
     if (idx >= total)
         return;
     const int cv = (int)(idx % CV);
@@ -282,8 +293,11 @@ maxpool_fixed_kernel(const T* __restrict__ x, T* __restrict__ y, int N, int H, i
     constexpr int ESZ = (int)sizeof(T);
     constexpr uint32_t OOB = 0x80000000u;
     const int CV = C / V;
+    uint32_t bid = blockIdx.x, grid = gridDim.x;
+    PPIPE_ARGS_NOW(bid, grid, "s"(x), "s"(y), "s"(N), "s"(H), "s"(W), "s"(C), "s"(Ho), "s"(Wo),
+                   "s"(pad));
     const uint32_t total = (uint32_t)N * Ho * Wo * CV;
-    const uint32_t idx = xcd_block() * 256u + threadIdx.x;
+    const uint32_t idx = xcd_block(bid, grid) * 256u + threadIdx.x;
     if (idx >= total)
         return;
     const int cv = (int)(idx % CV);
@@ -335,10 +349,12 @@ gap_kernel(const T* __restrict__ x, T* __restrict__ y, int N, int HW, int C)
     constexpr int ESZ = (int)sizeof(T);
     constexpr uint32_t OOB = 0x80000000u;
     __shared__ float part[16][16][V + 1];
+    uint32_t bid = blockIdx.x, grid = gridDim.x;
+    PPIPE_ARGS_NOW(bid, grid, "s"(x), "s"(y), "s"(N), "s"(HW), "s"(C));
     const int CV = C / V;
     const int cg = (CV + 15) / 16;
-    const int cv = blockIdx.x % cg * 16 + (threadIdx.x & 15);
-    const int n = blockIdx.x / cg;
+    const int cv = (int)bid % cg * 16 + (threadIdx.x & 15);
+    const int n = (int)bid / cg;
     const int pr = threadIdx.x >> 4;    // pixel row 0..15
     const auto xr = dw_rsrc(x, (uint32_t)N * HW * C * ESZ);
     float s[V];

@@ -205,7 +205,8 @@ __global__ void __launch_bounds__(PW_WAVES * 64) pw_conv_kernel(ConvGemmArgs a)
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int co0 = blockIdx.y * CF * 16;
+    const int3 bg = load_args_now(a, (int)blockIdx.x, (int)gridDim.x, (int)blockIdx.y);
+    const int co0 = bg.z * CF * 16;
     for (int i = tid; i < CF * 16; i += PW_WAVES * 64) {
         const bool in = co0 + i < a.Co;
         s_scale[i] = in ? a.scale[co0 + i] : 0.0f;
@@ -228,8 +229,8 @@ __global__ void __launch_bounds__(PW_WAVES * 64) pw_conv_kernel(ConvGemmArgs a)
     // input [M][C]: lane l reads pixel 16 g + l % 16, channels 32 ks + 8 (l / 16) .. + 8
     const auto xsrc = pw_rsrc(a.x, (uint32_t)a.M * a.C * ESZ);
     const int groups = (a.M + 15) / 16;
-    const int stride = gridDim.x * PW_WAVES;
-    int g = blockIdx.x * PW_WAVES + wave;
+    const int stride = bg.y * PW_WAVES;
+    int g = bg.x * PW_WAVES + wave;
     auto bload = [&](int gg, uint4 (&b)[KS]) {
         const int p = gg * 16 + (lane & 15);
 #pragma unroll
@@ -293,7 +294,8 @@ __global__ void __launch_bounds__(PW_WAVES * 64) stem_conv_kernel(ConvGemmArgs a
     const bool rows_out = a.Co % EPV == 0;
 
     const int tid = threadIdx.x, lane = tid & 63;
-    const int co0 = blockIdx.y * ROWS;
+    const int3 bg = load_args_now(a, (int)blockIdx.x, (int)gridDim.x, (int)blockIdx.y);
+    const int co0 = bg.z * ROWS;
     for (int i = tid; i < ROWS; i += PW_WAVES * 64) {
         const bool in = co0 + i < a.Co;
         s_scale[i] = in ? a.scale[co0 + i] : 0.0f;
@@ -311,10 +313,10 @@ __global__ void __launch_bounds__(PW_WAVES * 64) stem_conv_kernel(ConvGemmArgs a
     const auto xsrc = pw_rsrc(a.x, (uint32_t)a.N * a.H * a.W * a.C * ESZ);
     const int taps = a.KH * a.KW, hw = a.Ho * a.Wo;
     const int groups = (a.M + 15) / 16;
-    const int stride = gridDim.x * PW_WAVES;
+    const int stride = bg.y * PW_WAVES;
     const int q = lane >> 4, cl = 4 * q;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    for (int g = blockIdx.x * PW_WAVES + wave; g < groups; g += stride) {
+    for (int g = bg.x * PW_WAVES + wave; g < groups; g += stride) {
         const int p = g * 16 + (lane & 15);
         const int n = p / hw, rem = p - n * hw;
         const int ho = rem / a.Wo, wo = rem - (rem / a.Wo) * a.Wo;
