@@ -1479,6 +1479,9 @@ GemmCfgInfo gemm_cfg_info(int cfg)
     case GEMM_MX_256x128_S3: return {256, 128, 8, false, 3, 8, 32};
     case GEMM_MX_128x128_8W_S2: return {128, 128, 8, false, 2, 8, 32};
     case GEMM_MX_128x128_8W_S3: return {128, 128, 8, false, 3, 8, 32};
+    case GEMM_DMA_64x64_2W_S2: return {64, 64, 8, false, 2, 2};
+    case GEMM_DMA_64x64_1W_S2: return {64, 64, 8, false, 2, 1};
+    case GEMM_DMA_64x64_2W_S3: return {64, 64, 8, false, 3, 2};
     default:            return {0, 0, 0, false};
     }
 }
@@ -1621,6 +1624,9 @@ static hipError_t launch_cfg(int cfg, int wk, bool tapv, const ConvGemmArgs& a,
     case GEMM_MX_256x128_S3: return launch_mx<T, 256, 128, 4, 2, 3>(tapv, a, s);
     case GEMM_MX_128x128_8W_S2: return launch_mx<T, 128, 128, 2, 4, 2>(tapv, a, s);
     case GEMM_MX_128x128_8W_S3: return launch_mx<T, 128, 128, 2, 4, 3>(tapv, a, s);
+    case GEMM_DMA_64x64_2W_S2: return launch_dma<T, 64, 64, 1, 2, 2>(tapv, a, s);
+    case GEMM_DMA_64x64_1W_S2: return launch_dma<T, 64, 64, 1, 1, 2>(tapv, a, s);
+    case GEMM_DMA_64x64_2W_S3: return launch_dma<T, 64, 64, 1, 2, 3>(tapv, a, s);
     default:            return hipErrorInvalidValue;
     }
 }
@@ -1746,7 +1752,8 @@ const char* conv_gemm_name(int dt, int cfg, int wk, bool tapv)
                      c.waves, c.dma, tapv ? ",tapv" : "");
         else if (c.dma)
             snprintf(n, 64, "conv_gemm<%s,%dx%d,kv%d%s,dma%d%s>", dt_name(dt), c.bm, c.bn, c.kv,
-                     c.waves == 8 ? ",8w" : "", c.dma, tapv ? ",tapv" : "");
+                     c.waves == 8 ? ",8w" : c.waves == 2 ? ",2w" : c.waves == 1 ? ",1w" : "",
+                     c.dma, tapv ? ",tapv" : "");
         else
             snprintf(n, 64, "conv_gemm<%s,%dx%d,kv%d%s%s>", dt_name(dt), c.bm, c.bn, c.kv,
                      cfg == GEMM_128x128_8W ? ",8w" : "", tapv ? ",tapv" : "");

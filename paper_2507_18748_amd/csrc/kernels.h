@@ -131,7 +131,10 @@ enum GemmCfg : int {
     GEMM_MX_256x128_S3 = 26,
     GEMM_MX_128x128_8W_S2 = 27,   // 8 waves (2 x 4): 64x32 per wave
     GEMM_MX_128x128_8W_S3 = 28,
-    GEMM_NCFG = 29
+    GEMM_DMA_64x64_2W_S2 = 29,    // 2 waves, 64x32 per wave, 2 stages
+    GEMM_DMA_64x64_1W_S2 = 30,    // 1 wave, 64x64, 2 stages
+    GEMM_DMA_64x64_2W_S3 = 31,    // 2 waves, 3 stages, software-pipelined
+    GEMM_NCFG = 32
 };
 struct GemmCfgInfo {
     int bm, bn, kv;       // tile rows (co), columns (m); kv: 16-byte vectors of K per LDS stage

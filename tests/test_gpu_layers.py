@@ -300,6 +300,11 @@ FORCED = [  # (configuration id, waves, splits): every kernel variant the planne
     ("27,0,1", "conv_gemm_mx<", "128x128,8w,dma2"), ("27,0,3", "conv_gemm_mx<", "128x128,8w,dma2"),
     ("28,0,1", "conv_gemm_mx<", "128x128,8w,dma3"), ("28,0,2", "conv_gemm_mx<", "128x128,8w,dma3"),
 ]
+FORCED += [
+    ("29,0,1", "conv_gemm<", "64x64,kv8,2w,dma2"), ("29,0,3", "conv_gemm<", "64x64,kv8,2w,dma2"),
+    ("30,0,1", "conv_gemm<", "64x64,kv8,1w,dma2"), ("30,0,2", "conv_gemm<", "64x64,kv8,1w,dma2"),
+    ("31,0,1", "conv_gemm<", "64x64,kv8,2w,dma3"), ("31,0,3", "conv_gemm<", "64x64,kv8,2w,dma3"),
+]
 MX_FORCED = [f for f in FORCED if f[1] == "conv_gemm_mx<"]
 FORCED_SHAPES = {  # ragged M and Co, padded 3x3 taps, a 1x1 with a K tail, an FC + softmax
     "3x3": ((64, 13, 13), [conv("c", -1, 64, 100, 3, 1, 1)], 3, "normal"),
