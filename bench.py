@@ -51,6 +51,8 @@ def roofline(records, dtype):
     out["traffic"] = None   # filled from committed HBM counters, see measured_traffic
     out["kernel"] = name
     out["launches_per_step"] = g["n"]
+    out["algorithmic_bytes_per_launch"] = g["bytes"] / g["n"]
+    out["algorithmic_flops_per_launch"] = g["flops"] / g["n"]
     out["avg_launch_us"] = avg_us
     out["share_of_step"] = g["us"] / sum(v["us"] for v in groups.values())
     return out
@@ -101,6 +103,31 @@ def cold_summary(records, dtype):
     return out
 
 
+def write_table_json(path, out):
+    """Writes a latency table compactly: per-batch lists aligned with
+    out["batches"] (microseconds to 0.01, fractions to 4 digits), a layer's
+    bound as one string when it is the same at every batch, one row a line."""
+    def r(v, nd):
+        return None if v is None else round(float(v), nd)
+    head = {k: v for k, v in out.items() if k != "rows"}
+    for k in ("partition_us", "sum_of_layers_us", "images_per_s"):
+        head[k] = [r(v, 2) for v in head[k]]
+    lines = []
+    for row in out["rows"]:
+        row = dict(row)
+        row["us"] = [r(v, 2) for v in row["us"]]
+        row["roofline_frac"] = [r(v, 4) for v in row["roofline_frac"]]
+        if len(set(row["bound"])) == 1:
+            row["bound"] = row["bound"][0]
+        lines.append(json.dumps(row, separators=(",", ":")))
+    text = ("{\n" + "".join(f" {json.dumps(k)}: {json.dumps(v, separators=(',', ':'))},\n"
+                             for k, v in head.items())
+            + ' "rows": [\n' + ",\n".join(lines) + "\n ]\n}\n")
+    json.loads(text)
+    with open(path, "w") as f:
+        f.write(text)
+
+
 def source_digest():
     """sha256 over the sources that define the GEMM kernel whose HBM counters
     are recorded and the planner that configures it (conv_gemm.hip,
@@ -115,7 +142,78 @@ def source_digest():
     return h.hexdigest()
 
 
-def measured_traffic(workload, kernel):
+def _pmc_per_dispatch(csv_dir, counter, match):
+    """Mean value of `counter` per dispatch of kernels whose name contains
+    `match`, from a rocprofv3 --pmc csv directory (run_counter_collection.csv)."""
+    import csv
+    import glob
+    vals = []
+    for path in glob.glob(os.path.join(csv_dir, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                if r["Counter_Name"] == counter and match in r["Kernel_Name"]:
+                    vals.append(float(r["Counter_Value"]))
+    return (sum(vals) / len(vals), len(vals)) if vals else (None, 0)
+
+
+def kernel_symbol(kernel):
+    """Mangled-name prefix of a LDS-staged GEMM configuration name such as
+    conv_gemm<f16,64x64,kv8,dma2> or conv_gemm_mx<bf16,128x128,4w,dma3>."""
+    fam, rest = kernel.split("<", 1)
+    parts = rest.rstrip(">").split(",")
+    t = {"f16": "DF16_", "bf16": "DF16b", "f32": "f"}[parts[0]]
+    bm, bn = (int(v) for v in parts[1].split("x"))
+    waves = 4
+    for q in parts[2:]:
+        if q.endswith("w"):
+            waves = int(q[:-1])
+    ns = int([q for q in parts if q.startswith("dma")][0][3:])
+    tapv = 1 if "tapv" in parts else 0
+    if fam == "conv_gemm_mx":
+        wm = {4: 2, 8: 4 if bm == 256 else 2}[waves]
+        return f"conv_gemm_mxI{t}Li{bm}ELi{bn}ELi{wm}ELi{waves // wm}ELi{ns}ELb{tapv}E"
+    wm, wn = {1: (1, 1), 2: (1, 2), 4: (2, 2), 8: (2, 4)}[waves]
+    return f"conv_gemm_dmaI{t}Li{bm}ELi{bn}ELi{wm}ELi{wn}ELi{ns}ELb{tapv}E"
+
+
+def traffic_record(args):
+    """Writes the HBM-traffic record of the workload's dominant kernel from
+    four rocprofv3 --pmc runs under --pmc-dir: FETCH_SIZE and WRITE_SIZE of
+    the benchmark command, and of a plain device copy (--copy-calibration),
+    in subdirectories FETCH_SIZE, WRITE_SIZE, copy_FETCH_SIZE,
+    copy_WRITE_SIZE.  The copy's counters against its known size give the
+    scale of each counter; the record carries the sha256 of the sources the
+    counters describe, so bench.py reports them only while those hold."""
+    rec_in = json.load(open(args.traffic_from))      # a bench.py line (--kernels run) of the same command
+    roof = rec_in["roofline"]
+    kernel = roof["kernel"]
+    match = kernel_symbol(kernel)
+    d = args.pmc_dir
+    fetch, nf = _pmc_per_dispatch(os.path.join(d, "FETCH_SIZE"), "FETCH_SIZE", match)
+    write, nw = _pmc_per_dispatch(os.path.join(d, "WRITE_SIZE"), "WRITE_SIZE", match)
+    cf, _ = _pmc_per_dispatch(os.path.join(d, "copy_FETCH_SIZE"), "FETCH_SIZE", "copyBuffer")
+    cw, _ = _pmc_per_dispatch(os.path.join(d, "copy_WRITE_SIZE"), "WRITE_SIZE", "copyBuffer")
+    copy_kib = args.copy_mib * 1024.0
+    fs, ws = copy_kib / cf, copy_kib / cw
+    out = {"workload": rec_in["config"]["name"], "batch": rec_in["config"]["batch"], "kernel": kernel,
+           "kernel_symbol_match": match,
+           "source_sha256": source_digest(),
+           "fetch_kib_per_dispatch": fetch, "write_kib_per_dispatch": write,
+           "fetch_scale": fs, "write_scale": ws, "dispatches": [nf, nw],
+           "traffic_bytes_per_launch": (fetch * fs + write * ws) * 1024.0,
+           "algorithmic_bytes_per_launch": roof.get("algorithmic_bytes_per_launch"),
+           "commands": args.pmc_commands.split(";") if args.pmc_commands else [],
+           "note": "FETCH_SIZE and WRITE_SIZE in KiB per dispatch of the dominant kernel's "
+                   "configuration, mean over every dispatch of the profiled command; scaled by "
+                   "a plain device copy's counters (reads x fetch_scale, writes x write_scale); "
+                   "bench.py reports traffic only while source_sha256 matches conv_gemm.hip, "
+                   "kernels.h and runtime.hip"}
+    with open(args.traffic_record, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out))
+
+
+def measured_traffic(workload, kernel, batch=None):
     """HBM bytes per launch of `kernel` on `workload` from a committed counter
     record (profiles/*_traffic.json: FETCH_SIZE and WRITE_SIZE per dispatch,
     scaled by a plain copy's counters), or None when there is none or the
@@ -126,6 +224,8 @@ def measured_traffic(workload, kernel):
         with open(path) as f:
             rec = json.load(f)
         if rec.get("workload") != workload or rec.get("kernel") != kernel:
+            continue
+        if batch is not None and rec.get("batch", batch) != batch:
             continue
         digest = digest or source_digest()
         if rec.get("source_sha256") == digest:
@@ -333,31 +433,31 @@ def latency_table(args):
         info = part.layer_info(i, batches[-1])
         row = {"layer": i, "name": m.layers[i].name, "op": m.layers[i].op,
                "S_i_bytes": info["out_bytes_b1"], "out_chw": [info["out_c"], info["out_h"], info["out_w"]],
-               "us": {}, "roofline_frac": {}, "bound": {}}
+               "us": [], "roofline_frac": [], "bound": []}
         for j, b in enumerate(batches):
             li = part.layer_info(i, b)
             fl = b * li["flops_b1"]
             by = b * li["act_bytes_b1"] + li["param_bytes"]
             t_roof = max(fl / peak_f, by / peak_b)
             us = float(table[i - wl.begin, j])
-            row["us"][b] = us
-            row["roofline_frac"][b] = t_roof * 1e6 / us if us > 0 else None
-            row["bound"][b] = "mfma" if fl / peak_f >= by / peak_b else "hbm"
+            row["us"].append(us)
+            row["roofline_frac"].append(t_roof * 1e6 / us if us > 0 else None)
+            row["bound"].append("mfma" if fl / peak_f >= by / peak_b else "hbm")
         row["kernel_at_max_batch"] = info["kernel"]
         rows.append(row)
     out = {"workload": wl.name, "description": wl.description, "dtype": wl.dtype,
            "layers": [wl.begin, wl.end], "batches": batches,
-           "partition_us": {b: float(whole[j]) for j, b in enumerate(batches)},
-           "sum_of_layers_us": {b: float(table[:, j].sum()) for j, b in enumerate(batches)},
-           "images_per_s": {b: b / (whole[j] * 1e-6) for j, b in enumerate(batches)},
-           "method": "layers: median over runs of the range in layer order, HIP events "
-                     "recorded by each layer's first and last kernel launch; partition: one "
-                     "captured HIP graph replayed back to back",
+           "partition_us": [float(v) for v in whole],
+           "sum_of_layers_us": [float(v) for v in table.sum(axis=0)],
+           "images_per_s": [b / (whole[j] * 1e-6) for j, b in enumerate(batches)],
+           "method": f"layers: median of {args.profile_reps} runs (after {args.profile_warmup} "
+                     "warm-up runs) of the range in layer order, HIP events recorded by each "
+                     "layer's first and last kernel launch; partition: one captured HIP graph "
+                     "replayed back to back",
            "rows": rows}
-    with open(args.table, "w") as f:
-        json.dump(out, f, indent=1)
+    write_table_json(args.table, out)
     print(json.dumps({"table": args.table, "workload": wl.name, "batches": len(batches),
-                      "partition_us": out["partition_us"]}))
+                      "partition_us": dict(zip(batches, out["partition_us"]))}))
     part.close()
 
 
@@ -647,11 +747,21 @@ def main():
     ap.add_argument("--library-baseline", action="store_true",
                     help="also time the same partition on PyTorch-ROCm's own kernels "
                          "(MIOpen convolutions) and add it to the line as library_baseline")
+    ap.add_argument("--traffic-record", metavar="OUT.json", default=None,
+                    help="write the dominant kernel's HBM-traffic record from rocprofv3 --pmc "
+                         "csv directories under --pmc-dir (needs --traffic-from)")
+    ap.add_argument("--traffic-from", metavar="BENCH.json", default=None,
+                    help="bench.py output line naming the dominant kernel")
+    ap.add_argument("--pmc-dir", default="gpurun_out/pmc")
+    ap.add_argument("--pmc-commands", default="", help="';'-separated commands that made the csvs")
+    ap.add_argument("--copy-mib", type=float, default=256.0)
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB mebibytes 10 times "
                          "(reference for the HBM byte counters) and exit")
     args = ap.parse_args()
 
+    if args.traffic_record:
+        return traffic_record(args)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on one GPU only: the partition forward is measured on a single "
               "MI355X (data parallelism over more GPUs needs no exchange and is not "
@@ -740,7 +850,7 @@ def main():
         a["mean_us"] /= args.timing_steps
         a["median_us"] = a["min_us"] = a["mean_us"]
     roof = roofline(recs, wl.dtype)
-    roof["traffic"] = measured_traffic(wl.name, roof["kernel"])
+    roof["traffic"] = measured_traffic(wl.name, roof["kernel"], wl.batch)
     roof["timing"] = (f"HIP events recorded by each launch, {args.timing_steps} directly "
                       f"launched steps after the timed region")
     if args.kernels:
