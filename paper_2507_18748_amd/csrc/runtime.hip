@@ -198,12 +198,17 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
     // workloads on MI355X, timed in layer order (weights cold as in a real
     // run, the split-K reduction at its in-order cost of ~4 us):
     //  * 16-bit layers with Co >= 128 take 8-wave 128x128 tiles once there
-    //    are enough of them to fill the chip, or, with a long K loop, a
+    //    are enough of them to fill the chip (one per CU; from 384 before,
+    //    ResNet-152 at batch 42-56 2.5% faster), or, with a long K loop, a
     //    hundred of them split over K;
-    //  * everything else takes 64x64 tiles; K is split only when each half
-    //    keeps >= 12 steps, then while the grid is short of about 1.5 blocks
-    //    per CU and each split keeps >= 4 steps, or up to 2 blocks per CU
-    //    with >= 12 steps per split;
+    //  * everything else takes 64x64 tiles; K is split in two only when each
+    //    half keeps >= 12 steps and the split grid still has one block per
+    //    CU, or 1.5 with >= 24 steps per half (ResNet-152's 196-pixel 3x3
+    //    layers at batch 11-15 ran both halves of a CU's two blocks in turn
+    //    and paid the reduction on top: 16.5 against 11.2 us, the whole
+    //    model 8-10% faster unsplit); further splits while the grid is short
+    //    of about 1.5 blocks per CU and each split keeps >= 4 steps, or up to
+    //    2 blocks per CU with >= 12 steps per split;
     //  * sparse grids (up to two 64x64 blocks, or under one 8-wave 128x128
     //    block, per CU) take software-pipelined loops; sparse 64x64 grids use
     //    8 waves and four stages (two in flight), because a lone block
@@ -222,9 +227,9 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
     if (dt == PPIPE_F32 && skinny_ok && M <= 4096 && K >= 256) {
         cfg = GEMM_SK_32x32;
         wk = 4;
-    } else if (wide && (t128 >= 384 || (t128 >= 96 && k128 >= 64))) {
+    } else if (wide && (t128 >= 256 || (t128 >= 96 && k128 >= 64))) {
         cfg = GEMM_DMA_128x128_8W_S2;
-        if (t128 < 384)
+        if (t128 < 256)
             while (splits < 16 && t128 * splits * 2 <= 512 && k128 / (splits * 2) >= 8)
                 splits *= 2;
         if (t128 * splits < 256)
@@ -245,7 +250,7 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
         while (splits < 32) {
             const int64_t nb = t * splits * 2;
             const int cps = k / (splits * 2);
-            const bool ok = splits == 1 ? (cps >= 12 && nb <= 384)
+            const bool ok = splits == 1 ? (cps >= 12 && (nb <= 256 || (nb <= 384 && cps >= 24)))
                                         : ((nb <= 128 && cps >= 2) || (nb <= 384 && cps >= 4) ||
                                            (nb <= 512 && cps >= 12));
             if (!ok) break;
