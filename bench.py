@@ -103,6 +103,38 @@ def cold_summary(records, dtype):
     return out
 
 
+def launch_floor(n=200, reps=10):
+    """Per-launch time of back-to-back dependent kernels replayed from one
+    captured graph: n in-place adds on one element (a 1-block kernel that
+    loads and stores), and on 1 MiB (1024 blocks).  The floor every launch of
+    a partition pays before its own work."""
+    import torch
+    out = {"launches_per_graph": n}
+    for label, numel in (("1 element", 1), ("1 MiB", 1 << 18)):
+        x = torch.zeros(numel, dtype=torch.float32, device="cuda")
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            for _ in range(3):
+                x.add_(1.0)
+        torch.cuda.current_stream().wait_stream(s)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(n):
+                x.add_(1.0)
+        for _ in range(5):
+            g.replay()
+        torch.cuda.synchronize()
+        best = 1e9
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            g.replay()
+            torch.cuda.synchronize()
+            best = min(best, time.perf_counter() - t0)
+        out[f"us_per_launch_{label.replace(' ', '_')}"] = best * 1e6 / n
+    return out
+
+
 def write_table_json(path, out):
     """Writes a latency table compactly: per-batch lists aligned with
     out["batches"] (microseconds to 0.01, fractions to 4 digits), a layer's
@@ -755,6 +787,9 @@ def main():
     ap.add_argument("--pmc-dir", default="gpurun_out/pmc")
     ap.add_argument("--pmc-commands", default="", help="';'-separated commands that made the csvs")
     ap.add_argument("--copy-mib", type=float, default=256.0)
+    ap.add_argument("--launch-floor", action="store_true",
+                    help="only time graphs of 200 back-to-back dependent launches of tiny "
+                         "kernels (the per-launch floor under a partition) and exit")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB mebibytes 10 times "
                          "(reference for the HBM byte counters) and exit")
@@ -778,6 +813,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes": n * 4, "repeats": 10}))
+        return
+    if args.launch_floor:
+        print(json.dumps(launch_floor()))
         return
     import workloads as W
     from paper_2507_18748_amd import Partition

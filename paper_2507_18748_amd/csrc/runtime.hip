@@ -219,13 +219,25 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
     //    most 64 output channels with at least 512 such tiles (fewer operand
     //    bytes per FLOP: VGG-16 conv1_2 at batch 16 124 -> 108 us, ResNet-152's
     //    7x7 stem at batch 64 116 -> 93 us);
-    //  * small fp32 layers take the skinny kernel (no reduction pass).
+    //  * small fp32 layers take the skinny kernel (no reduction pass); so do
+    //    16-bit layers with a long K loop (>= 1024) whose 16x16 skinny grid
+    //    holds at least 128 pixels and fits one block per CU: ResNet-152's
+    //    196-pixel layer3 convolutions at batch 1, where 64x64 tiles leave 16
+    //    blocks (1x1, 6.5 -> 5.5 us) or 8 K splits and a reduction (3x3, 9.7
+    //    -> 7.2 us); the whole model 4% faster at batch 1.  Smaller grids
+    //    (layer4's 49 pixels) ran faster per layer but slower in a replayed
+    //    graph, and FC layers gained nothing.
     const bool wide = dt != PPIPE_F32 && Co >= 128;
     const int64_t t128 = tiles(GEMM_DMA_128x128_8W_S2);
     const int k128 = steps(GEMM_DMA_128x128_8W_S2);
     int cfg = GEMM_DMA_64x64_S2, wk = 0, splits = 1;
+    const int64_t sk16 = (int64_t)((M + 15) / 16) * ((Co + 15) / 16);
     if (dt == PPIPE_F32 && skinny_ok && M <= 4096 && K >= 256) {
         cfg = GEMM_SK_32x32;
+        wk = 4;
+    } else if (dt != PPIPE_F32 && skinny_ok && !split_free && K >= 1024 && M >= 128 &&
+               sk16 <= 256) {
+        cfg = GEMM_SK_16x16;
         wk = 4;
     } else if (wide && (t128 >= 256 || (t128 >= 96 && k128 >= 64))) {
         cfg = GEMM_DMA_128x128_8W_S2;

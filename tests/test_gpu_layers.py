@@ -269,6 +269,23 @@ def test_skinny_16x32(dtype):
     check(m, dtype, 2, kind="relu_normal")
 
 
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("ci,k,s", [(1024, 1, 1), (256, 3, 1), (256, 3, 2)])
+def test_planned_skinny_16x16_on_small_16bit_grids(dtype, ci, k, s):
+    """ResNet-152's layer3 shapes at batch 1 (196 output pixels, 256 output
+    channels, K of 1024 or 2304): the planner picks the 16x16 skinny tile on
+    four waves for 16-bit types, against the oracle."""
+    from paper_2507_18748_amd import Partition
+    h = 14 * s
+    m = make((ci, h, h), [conv("c", -1, ci, 256, k, s, k // 2, act="relu")])
+    with Partition(m.layers, W.model_params(m, 0, dtype, 0, 1), (ci, h, h), 0, 1, dtype,
+                   max_batch=2) as part:
+        assert "conv_gemm_skinny<" in part.layer_info(0, 1)["kernel"]
+        assert "16x16" in part.layer_info(0, 1)["kernel"]
+        assert "conv_gemm_skinny<" not in part.layer_info(0, 2)["kernel"]   # 392 pixels
+    check(m, dtype, 1)
+
+
 FORCED = [  # (configuration id, waves, splits): every kernel variant the planner can emit
     ("0,0,1", "conv_gemm<", "128x128"), ("0,0,4", "conv_gemm<", "128x128"),
     ("1,0,1", "conv_gemm<", "64x64"), ("1,0,3", "conv_gemm<", "64x64"),
