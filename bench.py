@@ -58,13 +58,16 @@ def roofline(records, dtype):
     return out
 
 
-def cold_summary(records, dtype):
+def cold_summary(records, dtype, copy_fit=None):
     """Roofline fractions from isolated-cold launches (caches swept before
     every repetition): per kernel family, HBM fraction bytes-weighted
     (sum of bytes / (peak x sum of time)) for memory-bound families and for
     GEMM launches the roofline puts on HBM, MFMA fraction FLOP-weighted for
     GEMM launches it puts on MFMA.  Launches moving < 16 MB are counted
-    separately as launch-bound."""
+    separately as launch-bound.  With a cold-copy fit (copy_reference), each
+    memory-bound family also reports, over its launches of at least 16 MB,
+    the time a plain device copy of the same bytes takes under the same
+    isolated-cold method, summed, over the family's time."""
     peak_f = PEAK_MFMA_TFLOPS[dtype] * 1e12
     peak_b = PEAK_HBM_GBS * 1e9
     fam = {}
@@ -77,7 +80,8 @@ def cold_summary(records, dtype):
             else:
                 name = "conv_gemm (HBM-bound launches)"
         g = fam.setdefault(name, {"us": 0.0, "bytes": 0.0, "flops": 0.0, "launches": 0,
-                                  "small_launches": 0, "us_big": 0.0, "bytes_big": 0.0})
+                                  "small_launches": 0, "us_big": 0.0, "bytes_big": 0.0,
+                                  "copy_us_big": 0.0})
         g["us"] += r["median_us"]
         g["bytes"] += r["bytes"]
         g["flops"] += r["flops"]
@@ -87,6 +91,8 @@ def cold_summary(records, dtype):
         else:
             g["us_big"] += r["median_us"]
             g["bytes_big"] += r["bytes"]
+            if copy_fit:
+                g["copy_us_big"] += copy_fit["t0_us"] + r["bytes"] / (copy_fit["gb_per_s"] * 1e3)
     out = {}
     for name, g in fam.items():
         if g["us"] <= 0:
@@ -99,6 +105,8 @@ def cold_summary(records, dtype):
             d["hbm_frac"] = g["bytes"] / (g["us"] * 1e-6 * peak_b)
             if g["us_big"] > 0:
                 d["hbm_frac_launches_over_16MB"] = g["bytes_big"] / (g["us_big"] * 1e-6 * peak_b)
+                if copy_fit:
+                    d["vs_cold_copy_launches_over_16MB"] = g["copy_us_big"] / g["us_big"]
         out[name] = d
     return out
 
@@ -133,6 +141,78 @@ def launch_floor(n=200, reps=10):
             best = min(best, time.perf_counter() - t0)
         out[f"us_per_launch_{label.replace(' ', '_')}"] = best * 1e6 / n
     return out
+
+
+def copy_reference(sizes_mb=(8, 16, 32, 64, 128, 256), reps=5):
+    """HBM fraction a plain device copy reaches under the isolated-cold
+    method (a 1 GiB read sweep before each repetition, evicting L2 and the
+    memory-side cache), and warm: the practical ceiling the memory-bound
+    kernels' isolated-cold fractions compare with.  Bytes moved = read +
+    write of the copy; median over `reps`."""
+    import torch
+    sweep = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+    out = {}
+    for mb in sizes_mb:
+        n = int(mb * 2 ** 20) // 8              # mb megabytes moved: half read, half written
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        res = {}
+        for mode in ("cold", "warm"):
+            ts = []
+            for _ in range(reps):
+                if mode == "cold":
+                    _ = sweep.sum()
+                else:
+                    dst.copy_(src)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                dst.copy_(src)
+                e1.record()
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1e-3)
+            t = sorted(ts)[len(ts) // 2]
+            res[f"{mode}_us"] = round(t * 1e6, 2)
+            res[f"{mode}_hbm_frac"] = 2 * n * 4 / t / (PEAK_HBM_GBS * 1e9)
+        out[f"{mb}MB"] = res
+        del src, dst
+    del sweep
+    torch.cuda.synchronize()
+    # least-squares fit of the cold copy time, t = t0 + bytes / bw, for the
+    # per-family comparison in cold_summary
+    xs = [float(k[:-2]) * 2 ** 20 for k in out]
+    ys = [v["cold_us"] for v in out.values()]
+    mx, my = sum(xs) / len(xs), sum(ys) / len(ys)
+    slope = sum((x - mx) * (y - my) for x, y in zip(xs, ys)) / sum((x - mx) ** 2 for x in xs)
+    out["cold_fit"] = {"t0_us": my - slope * mx, "gb_per_s": 1e-3 / slope}
+    return out
+
+
+def batch_sweep(part, max_batch, xd, out, stream, batches, steps=20, rounds=3):
+    """Partition latency and images/s at several batches on the benchmark's
+    handle: a graph captured per batch on the leading images of the same
+    input and output buffers, best of `rounds` runs of `steps` replays."""
+    import torch
+    res = {"batches": [], "ms_per_step": [], "images_per_s": []}
+    for b in batches:
+        if b > max_batch:
+            continue
+        part.capture(b, xd.data_ptr(), out.data_ptr())
+        for _ in range(5):
+            part.run(b, xd.data_ptr(), out.data_ptr(), stream)
+        torch.cuda.synchronize()
+        best = 1e9
+        for _ in range(rounds):
+            t0 = time.perf_counter()
+            for _ in range(steps):
+                part.run(b, xd.data_ptr(), out.data_ptr(), stream)
+            torch.cuda.synchronize()
+            best = min(best, (time.perf_counter() - t0) / steps)
+        res["batches"].append(b)
+        res["ms_per_step"].append(round(best * 1e3, 4))
+        res["images_per_s"].append(round(b / best, 1))
+    res["method"] = (f"one captured graph per batch on the bench handle, best of {rounds} runs of "
+                     f"{steps} back-to-back replays (wall clock)")
+    return res
 
 
 def write_table_json(path, out):
@@ -757,6 +837,9 @@ def main():
                     help="serve synthetic request streams with the adaptive batching "
                          "scheduler over the workload's measured table (--batches 1-B)")
     ap.add_argument("--requests", type=int, default=200000)
+    ap.add_argument("--sweep-batches", default="1,2,4,8,16,32,64", metavar="LIST",
+                    help="also time graph replays of the same handle at these batches "
+                         "(up to the workload's batch) and report images/s per batch; '' skips")
     ap.add_argument("--cold-reps", type=int, default=5,
                     help="isolated-cold repetitions per launch (caches swept before each); "
                          "0 skips")
@@ -917,7 +1000,12 @@ def main():
     }
     if args.cold_reps > 0:
         cold = part.profile_kernels_cold(wl.batch, reps=args.cold_reps)
-        result["isolated_cold"] = cold_summary(cold, wl.dtype)
+        cref = copy_reference()
+        result["isolated_cold"] = cold_summary(cold, wl.dtype, cref["cold_fit"])
+        result["isolated_cold"]["copy_reference"] = cref
+    if args.sweep_batches:
+        result["batch_sweep"] = batch_sweep(part, wl.batch, xd, out, sp,
+                                            parse_batches(args.sweep_batches))
     if args.library_baseline:
         print("[bench] timing the PyTorch-ROCm library baseline", file=sys.stderr, flush=True)
         part.run(wl.batch, xd.data_ptr(), out.data_ptr(), sp)

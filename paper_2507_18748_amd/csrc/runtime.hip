@@ -202,11 +202,13 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
     //    ResNet-152 at batch 42-56 2.5% faster), or, with a long K loop, a
     //    hundred of them split over K;
     //  * everything else takes 64x64 tiles; K is split in two only when each
-    //    half keeps >= 12 steps and the split grid still has one block per
-    //    CU, or 1.5 with >= 24 steps per half (ResNet-152's 196-pixel 3x3
-    //    layers at batch 11-15 ran both halves of a CU's two blocks in turn
-    //    and paid the reduction on top: 16.5 against 11.2 us, the whole
-    //    model 8-10% faster unsplit); further splits while the grid is short
+    //    half keeps >= 12 steps and the split grid has at most 192 blocks
+    //    (three quarters of the CUs), or 384 with >= 24 steps per half: a
+    //    split halves the K loop but adds a reduction launch (ResNet-152's
+    //    196-pixel 3x3 layers at batch 11-15 ran both halves of a CU's two
+    //    blocks in turn and paid the reduction on top, 16.5 against 11.2 us,
+    //    the whole model 8-10% faster unsplit; at batch 8-10, 100-136 tiles,
+    //    1.4-2.9% faster unsplit); further splits while the grid is short
     //    of about 1.5 blocks per CU and each split keeps >= 4 steps, or up to
     //    2 blocks per CU with >= 12 steps per split;
     //  * sparse grids (up to two 64x64 blocks, or under one 8-wave 128x128
@@ -262,7 +264,7 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
         while (splits < 32) {
             const int64_t nb = t * splits * 2;
             const int cps = k / (splits * 2);
-            const bool ok = splits == 1 ? (cps >= 12 && (nb <= 256 || (nb <= 384 && cps >= 24)))
+            const bool ok = splits == 1 ? (cps >= 12 && (nb <= 192 || (nb <= 384 && cps >= 24)))
                                         : ((nb <= 128 && cps >= 2) || (nb <= 384 && cps >= 4) ||
                                            (nb <= 512 && cps >= 12));
             if (!ok) break;
