@@ -1482,6 +1482,7 @@ GemmCfgInfo gemm_cfg_info(int cfg)
     case GEMM_DMA_64x64_2W_S2: return {64, 64, 8, false, 2, 2};
     case GEMM_DMA_64x64_1W_S2: return {64, 64, 8, false, 2, 1};
     case GEMM_DMA_64x64_2W_S3: return {64, 64, 8, false, 3, 2};
+    case GEMM_DMA_128x128_8W_S4: return {128, 128, 8, false, 4, 8};
     default:            return {0, 0, 0, false};
     }
 }
@@ -1627,6 +1628,7 @@ static hipError_t launch_cfg(int cfg, int wk, bool tapv, const ConvGemmArgs& a,
     case GEMM_DMA_64x64_2W_S2: return launch_dma<T, 64, 64, 1, 2, 2>(tapv, a, s);
     case GEMM_DMA_64x64_1W_S2: return launch_dma<T, 64, 64, 1, 1, 2>(tapv, a, s);
     case GEMM_DMA_64x64_2W_S3: return launch_dma<T, 64, 64, 1, 2, 3>(tapv, a, s);
+    case GEMM_DMA_128x128_8W_S4: return launch_dma<T, 128, 128, 2, 4, 4>(tapv, a, s);
     default:            return hipErrorInvalidValue;
     }
 }

@@ -134,7 +134,8 @@ enum GemmCfg : int {
     GEMM_DMA_64x64_2W_S2 = 29,    // 2 waves, 64x32 per wave, 2 stages
     GEMM_DMA_64x64_1W_S2 = 30,    // 1 wave, 64x64, 2 stages
     GEMM_DMA_64x64_2W_S3 = 31,    // 2 waves, 3 stages, software-pipelined
-    GEMM_NCFG = 32
+    GEMM_DMA_128x128_8W_S4 = 32,  // 8 waves, 4 stages (two in flight, one block per CU)
+    GEMM_NCFG = 33
 };
 struct GemmCfgInfo {
     int bm, bn, kv;       // tile rows (co), columns (m); kv: 16-byte vectors of K per LDS stage

@@ -197,10 +197,14 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
     // Fitted to per-layer sweeps of every plan over the five partition
     // workloads on MI355X, timed in layer order (weights cold as in a real
     // run, the split-K reduction at its in-order cost of ~4 us):
-    //  * 16-bit layers with Co >= 128 take 8-wave 128x128 tiles once there
-    //    are enough of them to fill the chip (one per CU; from 384 before,
-    //    ResNet-152 at batch 42-56 2.5% faster), or, with a long K loop, a
-    //    hundred of them split over K;
+    //  * 16-bit layers with Co >= 128 take 8-wave 128x128 tiles: with 192 to
+    //    255 of them (128 with K >= 1024) on the four-stage ring, one block
+    //    per CU with two stages in flight (ResNet-152's 14x14 layer3 at batch
+    //    64: 3x3 29.6 -> 23.2 us, 1x1 1024->256 17.5 -> 14.9 us against
+    //    64x64 tiles, the whole model 8.8% faster, batch 44-56 6-8%); from
+    //    256 of them on the two-stage ring, two blocks per CU (from 384
+    //    before, ResNet-152 at batch 42-56 2.5% faster); with a long K loop,
+    //    a hundred of them split over K;
     //  * everything else takes 64x64 tiles; K is split in two only when each
     //    half keeps >= 12 steps and the split grid has at most 192 blocks
     //    (three quarters of the CUs), or 384 with >= 24 steps per half: a
@@ -241,6 +245,8 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
                sk16 <= 256) {
         cfg = GEMM_SK_16x16;
         wk = 4;
+    } else if (wide && t128 < 256 && (t128 >= 192 || (t128 >= 128 && K >= 1024))) {
+        cfg = GEMM_DMA_128x128_8W_S4;
     } else if (wide && (t128 >= 256 || (t128 >= 96 && k128 >= 64))) {
         cfg = GEMM_DMA_128x128_8W_S2;
         if (t128 < 256)

@@ -321,6 +321,7 @@ FORCED += [
     ("29,0,1", "conv_gemm<", "64x64,kv8,2w,dma2"), ("29,0,3", "conv_gemm<", "64x64,kv8,2w,dma2"),
     ("30,0,1", "conv_gemm<", "64x64,kv8,1w,dma2"), ("30,0,2", "conv_gemm<", "64x64,kv8,1w,dma2"),
     ("31,0,1", "conv_gemm<", "64x64,kv8,2w,dma3"), ("31,0,3", "conv_gemm<", "64x64,kv8,2w,dma3"),
+    ("32,0,1", "conv_gemm<", "128x128,kv8,8w,dma4"), ("32,0,2", "conv_gemm<", "128x128,kv8,8w,dma4"),
 ]
 MX_FORCED = [f for f in FORCED if f[1] == "conv_gemm_mx<"]
 FORCED_SHAPES = {  # ragged M and Co, padded 3x3 taps, a 1x1 with a K tail, an FC + softmax
