@@ -769,10 +769,14 @@ def vgpu_report(args):
     out = {"workload": wl.name, "layers": [wl.begin, wl.end], "batches": batches,
            "shares": {}, "method": "k handles on k CU-masked streams (CU i in share (i/8) mod k), "
                                    "graphs replayed side by side; latency = elapsed / reps per "
-                                   "stream, HIP events on each stream"}
+                                   "stream, HIP events on each stream; each handle planned for "
+                                   + ("the whole device" if args.vgpu_whole_plans else
+                                      "its share's CUs (ppipe_partition_create_on_share)")}
     for k in (1, 2, 3, 4):
         parts = [Partition(m.layers, P, (m.in_c, m.in_h, m.in_w), wl.begin, wl.end, wl.dtype,
-                           max_batch=max(batches)) for _ in range(k)]
+                           max_batch=max(batches),
+                           cu_share_parts=None if args.vgpu_whole_plans else k)
+                 for _ in range(k)]
         streams = [stream_cu_share(j, k) for j in range(k)]
         ext = [torch.cuda.ExternalStream(st) for st in streams]
         info = parts[0].info
@@ -837,9 +841,13 @@ def main():
                     help="serve synthetic request streams with the adaptive batching "
                          "scheduler over the workload's measured table (--batches 1-B)")
     ap.add_argument("--requests", type=int, default=200000)
+    ap.add_argument("--vgpu-whole-plans", action="store_true",
+                    help="with --vgpu-out: plan every share's handle for the whole device "
+                         "(the default plans each for its share's CUs)")
     ap.add_argument("--sweep-batches", default="1,2,4,8,16,32,64", metavar="LIST",
                     help="also time graph replays of the same handle at these batches "
-                         "(up to the workload's batch) and report images/s per batch; '' skips")
+                         "(up to the workload's batch) and report images/s per batch; 'none' "
+                         "skips")
     ap.add_argument("--cold-reps", type=int, default=5,
                     help="isolated-cold repetitions per launch (caches swept before each); "
                          "0 skips")
@@ -1003,7 +1011,7 @@ def main():
         cref = copy_reference()
         result["isolated_cold"] = cold_summary(cold, wl.dtype, cref["cold_fit"])
         result["isolated_cold"]["copy_reference"] = cref
-    if args.sweep_batches:
+    if args.sweep_batches and args.sweep_batches != "none":
         result["batch_sweep"] = batch_sweep(part, wl.batch, xd, out, sp,
                                             parse_batches(args.sweep_batches))
     if args.library_baseline:

@@ -102,6 +102,9 @@ typedef struct {
     int64_t workspace_bytes;         /* device bytes of activation and split-K buffers */
     int32_t tuned;                   /* 1 when created with a planner override
                                         (ppipe_partition_create_tuned), else 0 */
+    int32_t cus;                     /* compute units the kernel grids were planned for:
+                                        the device's, or one CU share's
+                                        (ppipe_partition_create_on_share) */
 } ppipe_partition_info_t;
 
 typedef struct {
@@ -164,6 +167,19 @@ typedef struct {
 ppipe_partition* ppipe_partition_create_tuned(const ppipe_model_desc* desc,
                                               int32_t layer_begin, int32_t layer_end,
                                               int32_t dtype, const ppipe_tuning* tuning);
+
+/* ppipe_partition_create for a handle that will run on the streams of one of
+ * `parts` CU shares (ppipe_stream_create_cu_share(i, parts, ...), a virtual
+ * GPU of 1/parts, Sec. 5.3): the planner sizes every kernel grid for the
+ * compute units of one share instead of the whole device, as the paper
+ * profiles each virtual-GPU size on its own.  Outputs stay within the
+ * stated tolerances of the oracle; they can differ in the last bits from a
+ * handle planned for the whole device (other tiles, other K splits).
+ * parts = 1 is ppipe_partition_create.  NULL with PPIPE_E_INVALID for parts
+ * outside 1..8. */
+ppipe_partition* ppipe_partition_create_on_share(const ppipe_model_desc* desc,
+                                                 int32_t layer_begin, int32_t layer_end,
+                                                 int32_t dtype, int32_t parts);
 
 /* Forward pass of the range at batch size `batch` (1..max_batch).
  * in:  device pointer, [batch][in_h][in_w][in_c] in dtype (caller-owned).

@@ -57,7 +57,8 @@ class PartitionInfo(ctypes.Structure):
                 ("out_c", ctypes.c_int32), ("out_h", ctypes.c_int32), ("out_w", ctypes.c_int32),
                 ("out_dtype", ctypes.c_int32), ("in_bytes_per_image", ctypes.c_int64),
                 ("out_bytes_per_image", ctypes.c_int64), ("weight_bytes", ctypes.c_int64),
-                ("workspace_bytes", ctypes.c_int64), ("tuned", ctypes.c_int32)]
+                ("workspace_bytes", ctypes.c_int64), ("tuned", ctypes.c_int32),
+                ("cus", ctypes.c_int32)]
 
 
 class LayerInfo(ctypes.Structure):
@@ -140,6 +141,8 @@ def load_library() -> ctypes.CDLL:
     lib.ppipe_partition_create_tuned.restype = vp
     lib.ppipe_partition_create_tuned.argtypes = [ctypes.POINTER(ModelDesc), i32, i32, i32,
                                                  ctypes.POINTER(Tuning)]
+    lib.ppipe_partition_create_on_share.restype = vp
+    lib.ppipe_partition_create_on_share.argtypes = [ctypes.POINTER(ModelDesc), i32, i32, i32, i32]
     lib.ppipe_partition_run.restype = ctypes.c_int
     lib.ppipe_partition_run.argtypes = [vp, i32, vp, vp, vp]
     lib.ppipe_partition_run_static_scratch.restype = ctypes.c_int
@@ -384,11 +387,15 @@ class Partition:
     tuning: planner overrides for kernel tests and tuning sweeps, a dict of
       Tuning fields (gemm_plan=(cfg, waves, splits) sets the first three);
       None (the default) leaves every choice to the planner.
+    cu_share_parts: plan the kernel grids for one of this many CU shares
+      (the handle will run on stream_cu_share(i, cu_share_parts) streams);
+      None or 1 plans for the whole device.  Not combined with tuning.
     """
 
     def __init__(self, layers: Sequence, params: Dict[int, Dict[str, np.ndarray]],
                  in_chw: Sequence[int], begin: int, end: int, dtype: str,
-                 max_batch: int = 64, bn_eps: float = 1e-5, tuning: Optional[dict] = None):
+                 max_batch: int = 64, bn_eps: float = 1e-5, tuning: Optional[dict] = None,
+                 cu_share_parts: Optional[int] = None):
         self._lib = load_library()
         self.begin, self.end, self.dtype = begin, end, dtype
         keep: List[np.ndarray] = []
@@ -425,6 +432,8 @@ class Partition:
             d.bn_var = ptr(p.get("bn_var"))
         desc = ModelDesc(len(layers), arr, int(in_chw[0]), int(in_chw[1]), int(in_chw[2]),
                          int(max_batch))
+        if tuning and cu_share_parts not in (None, 1):
+            raise ValueError("tuning overrides plan for the whole device; drop cu_share_parts")
         if tuning:
             t = Tuning(-1, 0, 1, 0, 0, 0, 0, 0)
             for k, v in tuning.items():
@@ -439,6 +448,9 @@ class Partition:
                     raise ValueError(f"unknown tuning field {k!r}")
             h = self._lib.ppipe_partition_create_tuned(ctypes.byref(desc), begin, end,
                                                        DTYPES[dtype], ctypes.byref(t))
+        elif cu_share_parts is not None:
+            h = self._lib.ppipe_partition_create_on_share(ctypes.byref(desc), begin, end,
+                                                          DTYPES[dtype], int(cu_share_parts))
         else:
             h = self._lib.ppipe_partition_create(ctypes.byref(desc), begin, end, DTYPES[dtype])
         if not h:

@@ -149,6 +149,7 @@ struct GraphEntry {
 struct ppipe_partition {
     int begin = 0, end = 0, dtype = 0, max_batch = 64, device = 0;
     ppipe_tuning tune{-1, 0, 1, 0, 0, 0, 0, 0};   // planner overrides given at create
+    int cus = 256;                                // compute units the plans are sized for
     bool tuned = false;                           // any override active
     Shape in{}, out{};
     int out_dtype = 0;
@@ -187,8 +188,13 @@ namespace {
 // dtype, eligibility) so that the latency table, the benchmark and the
 // parity tests exercise the same launches.
 Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool stem_ok,
-                 bool split_free, const ppipe_tuning& tune)
+                 bool split_free, const ppipe_tuning& tune, int cus)
 {
+    // Grid-size thresholds below are stated for the 256 CUs of a whole
+    // MI355X and scale with the CUs the handle runs on (a CU share of a
+    // virtual GPU has fewer).
+    const int64_t C = cus;
+    auto at = [&](int64_t n256) { return n256 * C / 256; };
     auto tiles = [&](int cfg) {
         GemmCfgInfo c = gemm_cfg_info(cfg);
         return (int64_t)((M + c.bn - 1) / c.bn) * ((Co + c.bm - 1) / c.bm);
@@ -242,17 +248,17 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
         cfg = GEMM_SK_32x32;
         wk = 4;
     } else if (dt != PPIPE_F32 && skinny_ok && !split_free && K >= 1024 && M >= 128 &&
-               sk16 <= 256) {
+               sk16 <= C) {
         cfg = GEMM_SK_16x16;
         wk = 4;
-    } else if (wide && t128 < 256 && (t128 >= 192 || (t128 >= 128 && K >= 1024))) {
+    } else if (wide && t128 < C && (t128 >= at(192) || (t128 >= at(128) && K >= 1024))) {
         cfg = GEMM_DMA_128x128_8W_S4;
-    } else if (wide && (t128 >= 256 || (t128 >= 96 && k128 >= 64))) {
+    } else if (wide && (t128 >= C || (t128 >= at(96) && k128 >= 64))) {
         cfg = GEMM_DMA_128x128_8W_S2;
-        if (t128 < 256)
-            while (splits < 16 && t128 * splits * 2 <= 512 && k128 / (splits * 2) >= 8)
+        if (t128 < C)
+            while (splits < 16 && t128 * splits * 2 <= at(512) && k128 / (splits * 2) >= 8)
                 splits *= 2;
-        if (t128 * splits < 256)
+        if (t128 * splits < C)
             cfg = GEMM_DMA_128x128_8W_S3;
     } else if (split_free) {
         // the softmax kernel of an FC + softmax layer adds the partials as it
@@ -270,15 +276,16 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
         while (splits < 32) {
             const int64_t nb = t * splits * 2;
             const int cps = k / (splits * 2);
-            const bool ok = splits == 1 ? (cps >= 12 && (nb <= 192 || (nb <= 384 && cps >= 24)))
-                                        : ((nb <= 128 && cps >= 2) || (nb <= 384 && cps >= 4) ||
-                                           (nb <= 512 && cps >= 12));
+            const bool ok = splits == 1
+                                ? (cps >= 12 && (nb <= at(192) || (nb <= at(384) && cps >= 24)))
+                                : ((nb <= at(128) && cps >= 2) || (nb <= at(384) && cps >= 4) ||
+                                   (nb <= at(512) && cps >= 12));
             if (!ok) break;
             splits *= 2;
         }
-        if (t * splits <= 512)
+        if (t * splits <= at(512))
             cfg = GEMM_DMA_64x64_8W_S4;
-        else if (splits == 1 && Co <= 64 && tiles(GEMM_DMA_64x128_8W_S2) >= 512)
+        else if (splits == 1 && Co <= 64 && tiles(GEMM_DMA_64x128_8W_S2) >= at(512))
             cfg = GEMM_DMA_64x128_8W_S2;
     }
     //  * 16-bit 1x1 stride-1 layers with at most 32 input channels (or 160
@@ -1000,7 +1007,7 @@ int build(ppipe_partition* P, const ppipe_model_desc* d, int begin, int end, int
         for (int b = 1; b <= P->max_batch; ++b) {
             const int M = b * l.Ho * l.Wo;
             const Plan p = choose_plan(M, l.Co, l.K, dt, l.skinny_ok, l.pw_ok, l.stem_ok,
-                                       l.softmax, P->tune);
+                                       l.softmax, P->tune, P->cus);
             l.plans[b - 1] = p;
             size_t need = 0;
             if (p.splits > 1) need += (size_t)p.splits * M * l.Co;
@@ -1224,12 +1231,34 @@ ppipe_partition* ppipe_partition_create(const ppipe_model_desc* desc, int32_t la
     return ppipe_partition_create_tuned(desc, layer_begin, layer_end, dtype, nullptr);
 }
 
-ppipe_partition* ppipe_partition_create_tuned(const ppipe_model_desc* desc,
-                                              int32_t layer_begin, int32_t layer_end,
-                                              int32_t dtype, const ppipe_tuning* tuning)
+}   // extern "C"
+
+namespace {
+
+// Compute units of one of `parts` CU shares of the current device: the
+// device's CUs in groups of 8 dealt round-robin to the shares (as
+// ppipe_stream_create_cu_share deals them), the smallest share; 256 (one
+// MI355X) when the device cannot be queried.
+int share_cus(int parts)
+{
+    int cus = 256, dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        n > 0)
+        cus = n;
+    return std::max(8, cus / 8 / parts * 8);
+}
+
+ppipe_partition* create_partition(const ppipe_model_desc* desc, int32_t layer_begin,
+                                  int32_t layer_end, int32_t dtype, const ppipe_tuning* tuning,
+                                  int32_t parts)
 {
     g_err.clear();
     g_status = 0;
+    if (parts < 1 || parts > 8) {
+        fail(PPIPE_E_INVALID, "CU shares must be 1..8, got " + std::to_string(parts));
+        return nullptr;
+    }
     if (tuning) {
         const ppipe_tuning& t = *tuning;
         if (t.gemm_cfg < -1 || t.gemm_cfg >= GEMM_NCFG || t.gemm_splits < 0 ||
@@ -1266,6 +1295,7 @@ ppipe_partition* ppipe_partition_create_tuned(const ppipe_model_desc* desc,
     P->end = layer_end;
     P->dtype = dtype;
     P->max_batch = desc->max_batch > 0 ? desc->max_batch : 64;
+    P->cus = share_cus(parts);
     // host-side validation and packing first: a bad description fails
     // without touching the device
     if (build(P, desc, layer_begin, layer_end, dtype) != PPIPE_OK || allocate(P) != PPIPE_OK) {
@@ -1282,6 +1312,24 @@ ppipe_partition* ppipe_partition_create_tuned(const ppipe_model_desc* desc,
     // a failure)
     resolve_scratch(P->device);
     return P;
+}
+
+}  // namespace
+
+extern "C" {
+
+ppipe_partition* ppipe_partition_create_tuned(const ppipe_model_desc* desc,
+                                              int32_t layer_begin, int32_t layer_end,
+                                              int32_t dtype, const ppipe_tuning* tuning)
+{
+    return create_partition(desc, layer_begin, layer_end, dtype, tuning, 1);
+}
+
+ppipe_partition* ppipe_partition_create_on_share(const ppipe_model_desc* desc,
+                                                 int32_t layer_begin, int32_t layer_end,
+                                                 int32_t dtype, int32_t parts)
+{
+    return create_partition(desc, layer_begin, layer_end, dtype, nullptr, parts);
 }
 
 void ppipe_partition_destroy(ppipe_partition* h)
@@ -1737,6 +1785,7 @@ int ppipe_partition_info(const ppipe_partition* h, ppipe_partition_info_t* info)
     for (size_t b : h->slot_bytes) ws += b;
     info->workspace_bytes = (int64_t)ws;
     info->tuned = h->tuned ? 1 : 0;
+    info->cus = h->cus;
     return PPIPE_OK;
 }
 

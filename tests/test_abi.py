@@ -159,3 +159,17 @@ def test_create_tuned_rejects_out_of_range_overrides():
     with pytest.raises(ValueError):
         Partition(layers, _params(layers), (8, 6, 6), 0, 5, "f16", max_batch=4,
                   tuning={"no_such_field": 1})
+
+
+def test_create_on_share_rejects_out_of_range_parts():
+    """CU-share-sized planning takes 1..8 shares; the check comes before any
+    device work, and tuning overrides cannot be combined with it."""
+    from paper_2507_18748_amd import Partition
+    layers = _tiny_layers()
+    for bad in (0, 9, -1):
+        st = _status_of(lambda: Partition(layers, _params(layers), (8, 6, 6), 0, 5, "f16",
+                                          max_batch=4, cu_share_parts=bad))
+        assert st == -1, bad
+    with pytest.raises(ValueError):
+        Partition(layers, _params(layers), (8, 6, 6), 0, 5, "f16", max_batch=4,
+                  tuning={"no_pair": 1}, cu_share_parts=2)

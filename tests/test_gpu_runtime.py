@@ -137,6 +137,40 @@ def test_chained_blocks_match_the_whole_range_bitwise():
     np.testing.assert_array_equal(got.reshape(ref.shape), ref)
 
 
+@pytest.mark.parametrize("parts", [2, 4])
+def test_handles_planned_for_a_cu_share(parts):
+    """A handle created for one of `parts` CU shares plans its grids for that
+    share's compute units: fewer CUs in its info, K splits and tiles chosen
+    for them (some layer of ResNet-50 [44,56) at batch 8 changes plan), and
+    its output on a share stream matches the oracle at the end-to-end bar."""
+    import torch
+    from paper_2507_18748_amd import Partition, stream_cu_share, stream_destroy
+    wl, m, P = _small()
+    x = wl.input(8)
+    ref = oracle.forward(m.layers, P, wl.begin, wl.end, x, wl.dtype)
+    with Partition(m.layers, P, (3, 224, 224), wl.begin, wl.end, wl.dtype, max_batch=8) as whole:
+        whole_plans = [whole.layer_info(i, 8)["kernel"] for i in range(wl.begin, wl.end)]
+        whole_cus = whole.info["cus"]
+    st = stream_cu_share(0, parts)
+    try:
+        with Partition(m.layers, P, (3, 224, 224), wl.begin, wl.end, wl.dtype, max_batch=8,
+                       cu_share_parts=parts) as h:
+            assert h.info["cus"] == whole_cus // 8 // parts * 8
+            plans = [h.layer_info(i, 8)["kernel"] for i in range(wl.begin, wl.end)]
+            print("changed:", [(a, b) for a, b in zip(whole_plans, plans) if a != b])
+            assert plans != whole_plans
+            xd = upload_nhwc(x, wl.dtype)
+            o = empty_out(h, 8)
+            h.run(8, xd.data_ptr(), o.data_ptr(), st)
+            torch.cuda.synchronize()
+            got = o.float().cpu().numpy().transpose(0, 3, 1, 2).reshape(ref.shape)
+            assert rel_inf(got, ref) <= 2e-2
+            assert (got.reshape(8, -1).argmax(1) == ref.reshape(8, -1).argmax(1)).all()
+    finally:
+        torch.cuda.synchronize()
+        stream_destroy(st)
+
+
 @pytest.mark.parametrize("parts", [1, 2, 3, 4])
 def test_runs_on_cu_share_streams_match_the_default_stream(parts):
     """Virtual GPUs: each share's stream runs its own handle side by side
