@@ -1223,10 +1223,9 @@ conv_gemm_mx(ConvGemmArgs a)
 }
 
 // Split-K reduction: one thread per 4 output channels of one pixel, partials
-// summed in split order (bitwise deterministic), then the layer epilogue.
-// The loads of four splits are issued before the first add (a load past the
-// last split reads zeros through the range check and is not added), so the
-// split latencies overlap instead of adding up.
+// summed in split order (bitwise deterministic), then the layer epilogue.  A
+// load past the last split reads zeros through the range check and is not
+// added.
 template <typename T>
 __global__ void __launch_bounds__(256) splitk_reduce_kernel(ConvGemmArgs a)
 {
@@ -1235,22 +1234,47 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(ConvGemmArgs a)
     const uint32_t i = (uint32_t)g.x * 256u + threadIdx.x;
     if (i >= nvec)
         return;
-    const auto src = make_rsrc(a.partial, (uint32_t)a.splits * nvec * 16u);
-    const uint32_t plane = nvec * 16u;
-    floatx4 t = __builtin_bit_cast(floatx4, buf_load16(src, i * 16u));
-    for (int sp0 = 1; sp0 < a.splits; sp0 += 4) {
-        uint4 u[4];
-#pragma unroll
-        for (int d = 0; d < 4; ++d)
-            u[d] = buf_load16(src, sp0 + d < a.splits ? (uint32_t)(sp0 + d) * plane + i * 16u : OOB);
-#pragma unroll
-        for (int d = 0; d < 4; ++d)
-            if (sp0 + d < a.splits)
-                t += __builtin_bit_cast(floatx4, u[d]);
-    }
     const int co = (int)((i * 4u) % (uint32_t)a.Co);
     const int m = (int)((i * 4u) / (uint32_t)a.Co);
-    store_out4<T>(a, co, m, t);
+    // The epilogue's operands and the partials of up to 16 splits are all
+    // requested before the first addition, so a small grid (few pixels, many
+    // splits) waits for memory about once rather than once per few splits.
+    // The sum still runs in split order.
+    const float4 sc = *(const float4*)(a.scale + co);
+    const float4 bi = *(const float4*)(a.bias + co);
+    const size_t o = (size_t)m * a.Co + co;
+    float4 r = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if (a.res)
+        r = Vec4<T>::load((const T*)a.res + o);
+    const auto src = make_rsrc(a.partial, (uint32_t)a.splits * nvec * 16u);
+    const uint32_t plane = nvec * 16u;
+    constexpr int G = 16;
+    floatx4 t = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int sp0 = 0; sp0 < a.splits; sp0 += G) {
+        uint4 u[G];
+#pragma unroll
+        for (int d = 0; d < G; ++d)
+            u[d] = buf_load16(src, sp0 + d < a.splits ? (uint32_t)(sp0 + d) * plane + i * 16u : OOB);
+#pragma unroll
+        for (int d = 0; d < G; ++d) {
+            if (sp0 + d == 0)
+                t = __builtin_bit_cast(floatx4, u[0]);
+            else if (sp0 + d < a.splits)
+                t += __builtin_bit_cast(floatx4, u[d]);
+        }
+    }
+    float4 v = make_float4(t[0] * sc.x + bi.x, t[1] * sc.y + bi.y, t[2] * sc.z + bi.z,
+                           t[3] * sc.w + bi.w);
+    if (a.softmax) {
+        *(float4*)(a.logits + o) = v;
+        return;
+    }
+    if (a.res) {
+        v.x += r.x; v.y += r.y; v.z += r.z; v.w += r.w;
+    }
+    v.x = apply_act(v.x, a.act); v.y = apply_act(v.y, a.act);
+    v.z = apply_act(v.z, a.act); v.w = apply_act(v.w, a.act);
+    Vec4<T>::store((T*)a.y + o, v);
 }
 
 // Skinny implicit GEMM for layers with few output pixels.
