@@ -299,12 +299,10 @@ Plan choose_plan(int M, int Co, int K, int dt, bool skinny_ok, bool pw_ok, bool 
         splits = 1;
     }
     //  * stems of 3-channel images take the stem kernel (no channel-padding
-    //    pass): filters of up to 28 taps always (3x3 stems 1.7-2.4x faster),
-    //    7x7 stems only on small grids (its 13 k-steps of gathered taps
-    //    leave one wave per SIMD; the padded GEMM is ahead from about
-    //    200k output pixels).  The no_stem tuning override turns it off.
-    const int taps = K / (16 / dtype_size(dt));
-    if (stem_ok && (taps <= 28 || M <= 65536) && !tune.no_stem) {
+    //    pass): 3x3 stems 1.7-2.4x faster than the padded GEMM; ResNet-152's
+    //    7x7 stem as a whole model 0.3-3.6% faster at batch 6-32 and even from
+    //    40 to 64.  The no_stem tuning override turns it off.
+    if (stem_ok && !tune.no_stem) {
         cfg = GEMM_STEM;
         wk = stem_channel_frags(Co);
         splits = 1;
