@@ -70,21 +70,19 @@ def test_static_scratch_refuses_more_than_it_holds():
 
 
 def test_static_scratch_on_resnet152():
-    """ResNet-152 needs more than the array at batch 64 (the stem's
-    channel-padded input and layer4's split-K partials) and fits at 32."""
-    from paper_2507_18748_amd import Partition, PpipeError
+    """ResNet-152 (the default workload) fits the array at batch 64 (its
+    scratch is layer4's split-K partials; the stem kernel reads the
+    3-channel image as it is) and equals run() there and then at batch 32."""
+    from paper_2507_18748_amd import Partition
     wl = W.workload("resnet152")
     m = wl.build_model()
     P = wl.params(m)
     with Partition(m.layers, P, (m.in_c, m.in_h, m.in_w), wl.begin, wl.end, wl.dtype,
                    max_batch=64) as part:
+        assert part.layer_info(0, 64)["kernel"].startswith("stem_conv<")
         x = wl.input(64)
-        xd = upload_nhwc(x, wl.dtype)
-        o = empty_out(part, 64)
-        print("[no-alloc] resnet152 batch 64 refused", flush=True)
-        with pytest.raises(PpipeError) as e:
-            part.run_static_scratch(64, xd.data_ptr(), o.data_ptr(), 0)
-        assert e.value.status == -1
-        print("[no-alloc] resnet152 batch 32", flush=True)
-        ref, got = _run_both(part, x[:32], wl.dtype)
-        np.testing.assert_array_equal(got, ref)
+        for b in (64, 32):                      # the second call on a smaller batch
+            print(f"[no-alloc] resnet152 batch {b}", flush=True)
+            ref, got = _run_both(part, x[:b], wl.dtype)
+            assert np.isfinite(ref).all()
+            np.testing.assert_array_equal(got, ref)
