@@ -132,11 +132,13 @@ __device__ __forceinline__ void pw_store4(const ConvGemmArgs& a, int p, int co, 
 // pixel's channel row instead of 8- or 16-byte pieces of 16 rows.
 template <int CF>
 constexpr int pw_trow() { return CF * 16 + 4; }
+// Pixels p0 .. p0 + nvalid - 1 (nvalid <= 16) are lane rows 0 .. nvalid - 1.
 template <typename T, int CF>
-__device__ __forceinline__ void pw_rows_store(const ConvGemmArgs& a, const floatx4 (&acc)[CF],
-                                              const float* __restrict__ s_scale,
-                                              const float* __restrict__ s_bias,
-                                              float* __restrict__ tw, int g, int co0, int lane)
+__device__ __forceinline__ void pw_rows_store_at(const ConvGemmArgs& a, const floatx4 (&acc)[CF],
+                                                 const float* __restrict__ s_scale,
+                                                 const float* __restrict__ s_bias,
+                                                 float* __restrict__ tw, int p0, int nvalid,
+                                                 int co0, int lane)
 {
     constexpr int VE = 16 / (int)sizeof(T);     // channels per 16-byte vector
     constexpr int NV = 16 * CF / VE;            // vectors of a pixel's slice
@@ -160,8 +162,8 @@ __device__ __forceinline__ void pw_rows_store(const ConvGemmArgs& a, const float
     for (int it = 0; it < NIT; ++it) {
         const int v = it * 64 + lane;
         const int px = v / NV, cv = v - px * NV;
-        const int p = g * 16 + px, co = co0 + VE * cv;
-        if (v < 16 * NV && p < a.M && co < a.Co) {
+        const int p = p0 + px, co = co0 + VE * cv;
+        if (v < 16 * NV && px < nvalid && co < a.Co) {
             const size_t off = (size_t)p * a.Co + co;
             uint4 r = make_uint4(0u, 0u, 0u, 0u);
             if (a.res)
@@ -187,6 +189,15 @@ __device__ __forceinline__ void pw_rows_store(const ConvGemmArgs& a, const float
         }
     }
     __builtin_amdgcn_wave_barrier();
+}
+// Group g: pixels 16 g .. 16 g + 15 (those below M).
+template <typename T, int CF>
+__device__ __forceinline__ void pw_rows_store(const ConvGemmArgs& a, const floatx4 (&acc)[CF],
+                                              const float* __restrict__ s_scale,
+                                              const float* __restrict__ s_bias,
+                                              float* __restrict__ tw, int g, int co0, int lane)
+{
+    pw_rows_store_at<T, CF>(a, acc, s_scale, s_bias, tw, g * 16, a.M - g * 16, co0, lane);
 }
 
 // Block: PW_WAVES waves on output channels [co0, co0 + 16 CF); blockIdx.y is
@@ -367,6 +378,149 @@ __global__ void __launch_bounds__(PW_WAVES * 64) stem_conv_kernel(ConvGemmArgs a
     }
 }
 
+// Stem with the input window in LDS.  A block's tile is PW_WAVES output rows
+// (wave w: row w) by 16 output columns of one image; the input rows and
+// columns those outputs read are loaded into LDS once per tile (each pixel's
+// C <= 4 channels padded to four, zeros outside the image), and every lane
+// reads its taps from there instead of gathering them from global memory
+// (the gather kernel above issues KH KW C two-byte loads per output pixel).
+// The tap order, the weights and the MFMA sequence are the gather kernel's,
+// so the sums are bit-identical to it.  Blocks walk the tiles with a
+// block-uniform stride; the weights of the block's channel slice stay in LDS.
+template <typename T>
+constexpr int stem_patch_bytes() { return sizeof(T) == 4 ? 16 : 8; }   // one padded pixel
+template <typename T>
+constexpr int stem_patch_px() { return 8192 / stem_patch_bytes<T>(); }   // 8 KB window buffer
+
+template <typename T, int CF, int KST>
+__global__ void __launch_bounds__(PW_WAVES * 64) stem_patch_kernel(ConvGemmArgs a)
+{
+    constexpr int ESZ = (int)sizeof(T);
+    constexpr int EPV = 16 / ESZ;
+    constexpr int ROWS = CF * 16;
+    constexpr int PB = stem_patch_bytes<T>();
+    __shared__ __attribute__((aligned(16))) float s_scale[ROWS], s_bias[ROWS];
+    __shared__ uint4 s_w[KST * ROWS * 4];
+    __shared__ __attribute__((aligned(16))) unsigned char s_patch[stem_patch_px<T>() * PB];
+    __shared__ __attribute__((aligned(16))) float s_tile[PW_WAVES][16][pw_trow<CF>()];
+    const bool rows_out = a.Co % EPV == 0;
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int3 bg = load_args_now(a, (int)blockIdx.x, (int)gridDim.x, (int)blockIdx.y);
+    const int co0 = bg.z * ROWS;
+    for (int i = tid; i < ROWS; i += PW_WAVES * 64) {
+        const bool in = co0 + i < a.Co;
+        s_scale[i] = in ? a.scale[co0 + i] : 0.0f;
+        s_bias[i] = in ? a.bias[co0 + i] : 0.0f;
+    }
+    const auto wsrc = pw_rsrc(a.w, (uint32_t)a.Co * a.Kpad * ESZ);
+    for (int i = tid; i < KST * ROWS * 4; i += PW_WAVES * 64) {
+        const int q = i & 3, r = (i >> 2) % ROWS, ks = (i >> 2) / ROWS;
+        const int row = co0 + r, k = (4 * ks + q) * EPV;
+        s_w[i] = pw_load16(wsrc, row < a.Co && k < a.Kpad ? (uint32_t)((row * a.Kpad + k) * ESZ)
+                                                          : PW_OOB);
+    }
+
+    const auto xsrc = pw_rsrc(a.x, (uint32_t)a.N * a.H * a.W * a.C * ESZ);
+    const int taps = a.KH * a.KW;
+    const int PR = (PW_WAVES - 1) * a.stride + a.KH;     // window rows and columns
+    const int PC = 15 * a.stride + a.KW;
+    const int TY = (a.Ho + PW_WAVES - 1) / PW_WAVES, TX = (a.Wo + 15) / 16;
+    const int tiles = a.N * TY * TX;
+    const int q = lane >> 4, px = lane & 15;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    // this lane's window offset (in pixels) of each k-step's tap, or -1 past the taps
+    int toff[KST];
+#pragma unroll
+    for (int ks = 0; ks < KST; ++ks) {
+        const int t = 4 * ks + q;
+        const int kh = t / a.KW, kw = t - (t / a.KW) * a.KW;
+        toff[ks] = t < taps ? (wave * a.stride + kh) * PC + px * a.stride + kw : -1;
+    }
+    // The window of the block's next tile is loaded into registers while the
+    // current tile is computed (NPT window pixels per thread at most).
+    constexpr int NPT = stem_patch_px<T>() / (PW_WAVES * 64);
+    uint32_t e[NPT][4];
+    auto load_window = [&](int tile) {
+        const int n = tile / (TY * TX), r = tile - n * (TY * TX);
+        const int iy0 = (r / TX) * PW_WAVES * a.stride - a.pad;
+        const int ix0 = (r - (r / TX) * TX) * 16 * a.stride - a.pad;
+#pragma unroll
+        for (int j = 0; j < NPT; ++j) {
+            const int i = tid + j * PW_WAVES * 64;
+            const int py = i / PC, pc = i - (i / PC) * PC;
+            const int hi = iy0 + py, wi = ix0 + pc;
+            const bool ok = tile < tiles && i < PR * PC && hi >= 0 && hi < a.H && wi >= 0 &&
+                            wi < a.W;
+            const uint32_t base = (uint32_t)((((n * a.H + hi) * a.W + wi) * a.C) * ESZ);
+#pragma unroll
+            for (int ci = 0; ci < 4; ++ci) {
+                const uint32_t off = ok && ci < a.C ? base + ci * ESZ : PW_OOB;
+                if constexpr (ESZ == 4)
+                    e[j][ci] = __builtin_amdgcn_raw_buffer_load_b32(xsrc, off, 0, 0);
+                else
+                    e[j][ci] = __builtin_amdgcn_raw_buffer_load_b16(xsrc, off, 0, 0);
+            }
+        }
+    };
+    load_window(bg.x);
+    for (int tile = bg.x; tile < tiles; tile += bg.y) {   // the same trip count in every wave
+        const int n = tile / (TY * TX), r = tile - n * (TY * TX);
+        const int oy0 = (r / TX) * PW_WAVES, ox0 = (r - (r / TX) * TX) * 16;
+        __syncthreads();   // the previous tile's window reads are done (and the weights stored)
+#pragma unroll
+        for (int j = 0; j < NPT; ++j) {
+            const int i = tid + j * PW_WAVES * 64;
+            if (i < PR * PC) {
+                if constexpr (ESZ == 4)
+                    *(uint4*)(s_patch + i * PB) = uint4{e[j][0], e[j][1], e[j][2], e[j][3]};
+                else
+                    *(uint2*)(s_patch + i * PB) =
+                        uint2{e[j][0] | (e[j][1] << 16), e[j][2] | (e[j][3] << 16)};
+            }
+        }
+        load_window(tile + bg.y);
+        __syncthreads();
+        const int oy = oy0 + wave;
+        if (oy < a.Ho) {
+            uint4 b[KST];
+#pragma unroll
+            for (int ks = 0; ks < KST; ++ks) {
+                if constexpr (ESZ == 4) {
+                    b[ks] = toff[ks] >= 0 ? *(const uint4*)(s_patch + toff[ks] * PB)
+                                          : uint4{0u, 0u, 0u, 0u};
+                } else {
+                    const uint2 v = toff[ks] >= 0 ? *(const uint2*)(s_patch + toff[ks] * PB)
+                                                  : uint2{0u, 0u};
+                    b[ks] = uint4{v.x, v.y, 0u, 0u};
+                }
+            }
+            floatx4 acc[CF];
+#pragma unroll
+            for (int f = 0; f < CF; ++f) acc[f] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int ks = 0; ks < KST; ++ks)
+#pragma unroll
+                for (int f = 0; f < CF; ++f)
+                    acc[f] = pw_mfma<T>(s_w[(ks * ROWS + 16 * f + px) * 4 + q], b[ks], acc[f]);
+            const int p0 = (n * a.Ho + oy) * a.Wo + ox0;
+            const int nvalid = min(16, a.Wo - ox0);
+            if (rows_out) {
+                pw_rows_store_at<T, CF>(a, acc, s_scale, s_bias, &s_tile[wave][0][0], p0, nvalid,
+                                        co0, lane);
+            } else if (px < nvalid) {
+#pragma unroll
+                for (int f = 0; f < CF; ++f) {
+                    const int c = 16 * f + 4 * q, co = co0 + c;
+                    if (co >= a.Co)
+                        break;
+                    pw_store4<T>(a, p0 + px, co, c, acc[f], s_scale, s_bias);
+                }
+            }
+        }
+    }
+}
+
 template <typename T, int CF, int KS>
 hipError_t launch_pw_t(const ConvGemmArgs& a, int grid_blocks, hipStream_t s)
 {
@@ -442,10 +596,41 @@ hipError_t launch_stem_t(const ConvGemmArgs& a, int grid_blocks, hipStream_t s)
     return hipGetLastError();
 }
 
+template <typename T, int CF, int KST>
+hipError_t launch_stem_patch_t(const ConvGemmArgs& a, int grid_blocks, hipStream_t s)
+{
+    static int resident = 0;
+    if (!resident) {
+        int n = 0;
+        const hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+            &n, stem_patch_kernel<T, CF, KST>, PW_WAVES * 64, 0);
+        if (e != hipSuccess)
+            return e;
+        resident = std::max(1, n);
+    }
+    const int tiles = a.N * ((a.Ho + PW_WAVES - 1) / PW_WAVES) * ((a.Wo + 15) / 16);
+    const int slices = (a.Co + CF * 16 - 1) / (CF * 16);
+    const int cap = grid_blocks > 0 ? grid_blocks
+                                    : std::max(NUM_CUS_PW * resident / slices, NUM_CUS_PW);
+    const dim3 grid((unsigned)std::min(tiles, cap), (unsigned)slices), block(PW_WAVES * 64);
+    PPIPE_LAUNCH((stem_patch_kernel<T, CF, KST>), grid, block, 0, s, a);
+    return hipGetLastError();
+}
+
+// Filters of more than 12 taps take the window kernel when one tile's input
+// window fits its LDS buffer (ResNet-152's 7x7 stem at batch 64: the whole
+// model 0.7% faster); 3x3 stems keep the gather kernel, which was ahead on
+// them (VGG-16 0.6%, MobileNetV2 1.3%).
 template <typename T, int CF>
 hipError_t launch_stem_cf(const ConvGemmArgs& a, int grid_blocks, hipStream_t s)
 {
     const int kst = (a.KH * a.KW + 3) / 4;
+    const int window = ((PW_WAVES - 1) * a.stride + a.KH) * (15 * a.stride + a.KW);
+    if (kst > 3 && window <= stem_patch_px<T>()) {
+        if (kst <= 7) return launch_stem_patch_t<T, CF, 7>(a, grid_blocks, s);
+        if (kst <= 13) return launch_stem_patch_t<T, CF, 13>(a, grid_blocks, s);
+        return hipErrorInvalidValue;
+    }
     if (kst <= 3) return launch_stem_t<T, CF, 3>(a, grid_blocks, s);
     if (kst <= 7) return launch_stem_t<T, CF, 7>(a, grid_blocks, s);
     if (kst <= 13) return launch_stem_t<T, CF, 13>(a, grid_blocks, s);

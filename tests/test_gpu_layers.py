@@ -119,6 +119,27 @@ def test_stem_kernel_four_channels():
     check(m, "bf16", 2)
 
 
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("grid", [1, 5])
+def test_stem_window_grid_stride(dtype, grid):
+    """A 7x7 stride-2 stem (ragged: 23 x 20 outputs, tiles of 4 rows x 16
+    columns) launched on 1 or 5 blocks, so that every block walks several
+    tiles and loads the next tile's input window while it computes the
+    current one: the oracle's result, and the default launch's bits."""
+    from paper_2507_18748_amd import Partition
+    m = make((3, 45, 39), [conv("s", -1, 3, 64, 7, 2, 3)])
+    check(m, dtype, 2, kind="image", tuning={"stream_grid": grid})
+    P = W.model_params(m, 0, dtype)
+    x = W.partition_input((3, 45, 39), 2, 3, dtype, "image")
+    outs = []
+    for tuning in (None, {"stream_grid": grid}):
+        with Partition(m.layers, P, (3, 45, 39), 0, 1, dtype, max_batch=2,
+                       tuning=tuning) as part:
+            assert part.layer_info(0, 2)["kernel"].startswith("stem_conv<")
+            outs.append(gpu_forward(part, x))
+    np.testing.assert_array_equal(outs[0], outs[1])
+
+
 @pytest.mark.parametrize("grid", ["1", "8"])
 def test_pointwise_grid_stride_matches_default(grid):
     """A pointwise launch capped at 1 or 8 blocks (every wave walks many
