@@ -553,6 +553,8 @@ __device__ __forceinline__ void dma_wait()
     static_assert(N >= 0 && N < 64, "vmcnt range");
     asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
 }
+// Wait until every LDS read this wave issued has returned its data.
+__device__ __forceinline__ void lds_read_drain() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
 
 // ---- prefetched single-pass epilogue (LDS-staged kernels) ----------------
@@ -912,6 +914,161 @@ conv_gemm_dma(ConvGemmArgs a)
 {
     const int3 g = load_args_now(a, (int)blockIdx.x, (int)gridDim.x);
     conv_gemm_dma_body<T, BM, BN, WM, WN, NS, TAPV>(a, g.x, g.y);
+}
+
+// Warp-specialised variant of the 16-bit 128 x 128 eight-wave tile (plain
+// taps, one K split, the one-pass epilogue): NP more waves issue every
+// LDS-direct load and the eight MFMA waves only read fragments and multiply,
+// so the loads of later stages no longer wait in the MFMA waves' instruction
+// stream.  One barrier per stage: before barrier s the load waves have waited
+// for stage s and the MFMA waves have drained their reads of stage s - 1;
+// after it the load waves refill the slot of stage s - 1 with stage
+// s + NS - 1.  Every wave passes the same nst + 1 barriers of the K loop and
+// the two of the epilogue.
+template <typename T, int NS, int NP>
+__global__ void __launch_bounds__((8 + NP) * 64)
+conv_gemm_ws(ConvGemmArgs a)
+{
+    constexpr int BM = 128, BN = 128, WM = 2, WN = 4, NW = WM * WN;
+    constexpr int ESZ = (int)sizeof(T);
+    static_assert(ESZ == 2, "16-bit operands");
+    constexpr int EPV = 16 / ESZ;
+    constexpr int KV = 8, BK = KV * EPV, ROW = KV * 16;
+    constexpr int STAGE = (BM + BN) * ROW;
+    constexpr int WTM = BM / WM, WTN = BN / WN, FM = WTM / 16, FN = WTN / 16;
+    constexpr int PA = BM / (8 * NP), PB = BN / (8 * NP), PP = PA + PB;   // loads per load wave and stage
+    static_assert(BM % (8 * NP) == 0 && BN % (8 * NP) == 0, "whole 8-row groups per load wave");
+    static_assert(NS >= 3 && (NS - 2) * PP < 64, "ring depth");
+
+    extern __shared__ __attribute__((aligned(16))) unsigned char dyn_smem[];
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)dyn_smem;
+    const int3 g = load_args_now(a, (int)blockIdx.x, (int)gridDim.x);
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int3 tt = tile_of_block(a, g.x, g.y);
+    const int m0 = tt.x * BN, co0 = tt.y * BM;
+    const int nst = a.total_chunks;                 // one K split
+
+    floatx4 acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+            acc[i][j] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+    const int wm = wave % WM, wn = (wave / WM) % WN;
+
+    if (wave >= NW) {
+        // ---- load waves: load i of load wave w fills rows 8 (i NP + w) .. + 8
+        const int pw = wave - NW;
+        const auto wsrc = make_rsrc(a.w, (uint32_t)a.Co * a.Kpad * ESZ);
+        const auto xsrc = make_rsrc(a.x, (uint32_t)a.N * a.H * a.W * a.C * ESZ);
+        const int lr = lane >> 3, lp = lane & 7;
+        uint32_t a_off[PA];
+#pragma unroll
+        for (int i = 0; i < PA; ++i) {
+            const int row = 8 * (i * NP + pw) + lr;
+            const int kv = lp ^ dma_swz(row);
+            a_off[i] = co0 + row < a.Co ? (uint32_t)(((co0 + row) * a.Kpad + kv * EPV) * ESZ) : OOB;
+        }
+        PixelRow b_px[PB];
+        int b_k[PB];
+#pragma unroll
+        for (int i = 0; i < PB; ++i) {
+            const int row = 8 * (i * NP + pw) + lr;
+            b_px[i] = pixel_row(a, m0 + row, ESZ);
+            b_k[i] = lp ^ dma_swz(row);
+        }
+        TapCursor cur;
+        int lst = 0;
+        cur.start(0, a.C, a.KW);
+        // a stage past the end of K loads nothing (offset OOB): every call issues PP loads
+        auto issue = [&](uint32_t slot) {
+            const bool live = lst < nst;
+            const uint32_t k0b = (uint32_t)(lst * BK * ESZ);
+#pragma unroll
+            for (int i = 0; i < PA; ++i)
+                dma16(wsrc, live ? a_off[i] + k0b : OOB, slot + (i * NP + pw) * 8 * ROW);
+            const uint32_t bslot = slot + BM * ROW;
+            const int tap_off = ((cur.kh * a.W + cur.kw) * a.C + cur.ci) * ESZ;
+            const int cleft = a.C - cur.ci;
+#pragma unroll
+            for (int i = 0; i < PB; ++i) {
+                const bool ok = live &&
+                                ((b_px[i].hmask >> cur.kh) & (b_px[i].wmask >> cur.kw) & 1u) &&
+                                b_k[i] * EPV < cleft;
+                dma16(xsrc, ok ? (uint32_t)(b_px[i].off + tap_off + b_k[i] * 16) : OOB,
+                      bslot + (i * NP + pw) * 8 * ROW);
+            }
+            if (live) {
+                ++lst;
+                cur.advance(BK, a.C, a.KW);
+            }
+        };
+#pragma unroll
+        for (int p = 0; p < NS - 1; ++p)
+            issue(lds0 + p * STAGE);
+        int wr = NS - 1;   // slot that receives stage s + NS - 1
+        for (int s = 0; s < nst; ++s) {
+            dma_wait<(NS - 2) * PP>();   // stage s has landed (s + 1 .. s + NS - 2 may not)
+            bare_barrier();              // barrier s
+            issue(lds0 + wr * STAGE);    // the slot of stage s - 1
+            wr = wr + 1 == NS ? 0 : wr + 1;
+        }
+        dma_wait<0>();   // the tail loads (zeros past K) have landed before the ring is reused
+    } else {
+        // ---- MFMA waves
+        const int sw = (lane >> 4) ^ dma_swz(lane & 15);
+        int fa[FM], fb[FN];
+#pragma unroll
+        for (int i = 0; i < FM; ++i) fa[i] = (wm * WTM + i * 16 + (lane & 15)) * ROW + sw * 16;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) fb[j] = (BM + wn * WTN + j * 16 + (lane & 15)) * ROW + sw * 16;
+        int rd = 0;
+        for (int s = 0; s < nst; ++s) {
+            bare_barrier();   // barrier s: stage s has landed
+            const unsigned char* S = dyn_smem + rd * STAGE;
+            uint4 af[KV / 4][FM], bf[KV / 4][FN];
+#pragma unroll
+            for (int ks = 0; ks < KV / 4; ++ks) {
+#pragma unroll
+                for (int i = 0; i < FM; ++i) af[ks][i] = *(const uint4*)(S + (fa[i] ^ (ks * 64)));
+#pragma unroll
+                for (int j = 0; j < FN; ++j) bf[ks][j] = *(const uint4*)(S + (fb[j] ^ (ks * 64)));
+            }
+#pragma unroll
+            for (int ks = 0; ks < KV / 4; ++ks)
+#pragma unroll
+                for (int i = 0; i < FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < FN; ++j)
+                        Mfma<T>::step(af[ks][i], bf[ks][j], acc[i][j]);
+            __builtin_amdgcn_sched_group_barrier(0x100, (KV / 4) * (FM + FN), 0);   // LDS reads
+            __builtin_amdgcn_sched_group_barrier(0x008, (KV / 4) * FM * FN, 0);     // then MFMAs
+            lds_read_drain();   // this wave's reads of stage s are done before barrier s + 1
+            rd = rd + 1 == NS ? 0 : rd + 1;
+        }
+    }
+    bare_barrier();   // the loop's last barrier: every read done, every load landed
+
+    // ---- one-pass epilogue by the MFMA waves; the load waves take its barriers
+    constexpr int LROW = BM + 4;
+    EpiPre<T, BM, BN, NW * 64> epre;
+    if (wave < NW)
+        epre.load(a, m0, co0, tid);
+    float* ept = (float*)dyn_smem;
+    __syncthreads();
+    if (wave < NW) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+                *(floatx4*)(ept + (wn * WTN + j * 16 + (lane & 15)) * LROW + wm * WTM + i * 16 +
+                            4 * (lane >> 4)) = acc[i][j];
+    }
+    __syncthreads();
+    if (wave < NW)
+        epre.template finish<LROW>(a, ept, m0, co0, tid);
 }
 
 // Two independent layers of one tile configuration in one launch: blocks
@@ -1592,6 +1749,19 @@ static hipError_t launch_dma(bool tapv, const ConvGemmArgs& a, hipStream_t s)
                 : launch_dma_one<T, BM, BN, WM, WN, NS, false>(a, s);
 }
 
+template <typename T, int NS, int NP>
+static hipError_t launch_ws(const ConvGemmArgs& a, hipStream_t s)
+{
+    constexpr int bytes = gemm_lds_bytes(128, 128, NS);
+    static const hipError_t attr = hipFuncSetAttribute(
+        (const void*)conv_gemm_ws<T, NS, NP>, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (attr != hipSuccess)
+        return attr;
+    PPIPE_LAUNCH((conv_gemm_ws<T, NS, NP>), dim3((unsigned)(a.tiles_m * a.tiles_co)),
+                 dim3((8 + NP) * 64), bytes, s, a);
+    return hipGetLastError();
+}
+
 template <typename T, int FM, int FN>
 static hipError_t launch_skinny(int wk, const ConvGemmArgs& a, hipStream_t s)
 {
@@ -1652,7 +1822,11 @@ static hipError_t launch_cfg(int cfg, int wk, bool tapv, const ConvGemmArgs& a,
     case GEMM_DMA_64x64_2W_S2: return launch_dma<T, 64, 64, 1, 2, 2>(tapv, a, s);
     case GEMM_DMA_64x64_1W_S2: return launch_dma<T, 64, 64, 1, 1, 2>(tapv, a, s);
     case GEMM_DMA_64x64_2W_S3: return launch_dma<T, 64, 64, 1, 2, 3>(tapv, a, s);
-    case GEMM_DMA_128x128_8W_S4: return launch_dma<T, 128, 128, 2, 4, 4>(tapv, a, s);
+    case GEMM_DMA_128x128_8W_S4:
+        if constexpr (sizeof(T) == 2)
+            if (!tapv && a.splits == 1 && !a.softmax && a.Co % 8 == 0)
+                return launch_ws<T, 4, 8>(a, s);
+        return launch_dma<T, 128, 128, 2, 4, 4>(tapv, a, s);
     default:            return hipErrorInvalidValue;
     }
 }
