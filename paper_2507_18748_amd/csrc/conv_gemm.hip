@@ -925,11 +925,11 @@ conv_gemm_dma(ConvGemmArgs a)
 // after it the load waves refill the slot of stage s - 1 with stage
 // s + NS - 1.  Every wave passes the same nst + 1 barriers of the K loop and
 // the two of the epilogue.
-template <typename T, int NS, int NP>
-__global__ void __launch_bounds__((8 + NP) * 64)
+template <typename T, int BM, int BN, int WM, int WN, int NS, int NP>
+__global__ void __launch_bounds__((WM * WN + NP) * 64)
 conv_gemm_ws(ConvGemmArgs a)
 {
-    constexpr int BM = 128, BN = 128, WM = 2, WN = 4, NW = WM * WN;
+    constexpr int NW = WM * WN;
     constexpr int ESZ = (int)sizeof(T);
     static_assert(ESZ == 2, "16-bit operands");
     constexpr int EPV = 16 / ESZ;
@@ -1749,16 +1749,17 @@ static hipError_t launch_dma(bool tapv, const ConvGemmArgs& a, hipStream_t s)
                 : launch_dma_one<T, BM, BN, WM, WN, NS, false>(a, s);
 }
 
-template <typename T, int NS, int NP>
+template <typename T, int BM, int BN, int WM, int WN, int NS, int NP>
 static hipError_t launch_ws(const ConvGemmArgs& a, hipStream_t s)
 {
-    constexpr int bytes = gemm_lds_bytes(128, 128, NS);
+    constexpr int bytes = gemm_lds_bytes(BM, BN, NS);
     static const hipError_t attr = hipFuncSetAttribute(
-        (const void*)conv_gemm_ws<T, NS, NP>, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+        (const void*)conv_gemm_ws<T, BM, BN, WM, WN, NS, NP>,
+        hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
     if (attr != hipSuccess)
         return attr;
-    PPIPE_LAUNCH((conv_gemm_ws<T, NS, NP>), dim3((unsigned)(a.tiles_m * a.tiles_co)),
-                 dim3((8 + NP) * 64), bytes, s, a);
+    PPIPE_LAUNCH((conv_gemm_ws<T, BM, BN, WM, WN, NS, NP>), dim3((unsigned)(a.tiles_m * a.tiles_co)),
+                 dim3((WM * WN + NP) * 64), bytes, s, a);
     return hipGetLastError();
 }
 
@@ -1825,7 +1826,7 @@ static hipError_t launch_cfg(int cfg, int wk, bool tapv, const ConvGemmArgs& a,
     case GEMM_DMA_128x128_8W_S4:
         if constexpr (sizeof(T) == 2)
             if (!tapv && a.splits == 1 && !a.softmax && a.Co % 8 == 0)
-                return launch_ws<T, 4, 8>(a, s);
+                return launch_ws<T, 128, 128, 2, 4, 4, 8>(a, s);
         return launch_dma<T, 128, 128, 2, 4, 4>(tapv, a, s);
     default:            return hipErrorInvalidValue;
     }
