@@ -143,6 +143,34 @@ def _check_segments(name, batch, sample=None):
           f"worst rel_inf {worst:.2e}", flush=True)
 
 
+def _check_segments_at_batch(name, batch, sample):
+    """Element-wise parity of every minimal segment in the launch configuration
+    of `batch` (the plans the benchmark times), on sampled images: the oracle
+    computes the sampled images only; the other rows of each segment's input
+    repeat the first sample (each image is computed independently)."""
+    wl, m, P = _setup(name)
+    xs = wl.input(batch)[list(sample)]
+    _, outs = oracle.forward(m.layers, P, wl.begin, wl.end, xs, wl.dtype, keep=True)
+    cuts = [wl.begin] + boundaries(m.layers, wl.begin, wl.end) + [wl.end]
+    rows = list(sample)
+    worst = 0.0
+    for a, b in zip(cuts[:-1], cuts[1:]):
+        src = outs[a - 1]
+        xin = np.repeat(src[:1], batch, axis=0)
+        xin[rows] = src
+        with _partition(m, P, a, b, wl.dtype, batch) as part:
+            got = gpu_forward(part, xin)
+        ref = outs[b - 1]
+        got = got.reshape((batch,) + ref.shape[1:])[rows]
+        e = rel_inf(got, ref)
+        worst = max(worst, e)
+        print(f"    segment [{a},{b}) {m.layers[a].name}..{m.layers[b - 1].name} at batch {batch}: "
+              f"rel_inf {e:.2e}", flush=True)
+        assert e <= SEG_TOL[wl.dtype], f"segment [{a},{b}) rel_inf {e:.3e}"
+    print(f"[segment-parity] {name} batch {batch}, images {rows}: {len(cuts) - 1} segments, "
+          f"worst rel_inf {worst:.2e}", flush=True)
+
+
 # ---- end to end ----
 
 def test_resnet18_stem_layer1_fp32_batch1():
@@ -208,3 +236,9 @@ def test_segments_mobilenet_v2():
 
 def test_segments_resnet152_batch16():
     _check_segments("resnet152", 16)
+
+
+def test_segments_resnet152_batch64_sampled():
+    """The benchmark's configuration (ResNet-152 fp16 at batch 64), segment by
+    segment, on the first and last image."""
+    _check_segments_at_batch("resnet152", 64, (0, 63))
